@@ -1,0 +1,37 @@
+"""CPU oracle for the greedy speculative verification step.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+link this package: it is used by the tests, by ``__graft_entry__.smoke()`` to
+check one small GPU run, and by ``bench.py``'s CPU-baseline timing.  It shares
+no code with the HIP implementation; the only thing both sides consume is the
+seeded input generators in ``workloads``.
+
+What it computes (all arithmetic in float64):
+
+* ``model.forward_block`` - the target model's forward over a block of rows
+  appended to a committed KV cache: Eq. 3 (the draft appended to the prefix
+  and scored in one forward) over the decoder-only architecture the synthetic
+  targets use (RMSNorm, rotary positions, grouped-query attention, SwiGLU).
+  For bf16 models the values a bf16 pipeline stores are rounded to bf16
+  (round-to-nearest-even) at the points listed in ``model``; every other
+  quantity stays float64.
+* ``accept`` - greedy decoding of each row (Sec. "Reuse", the decode function
+  of Eq. 7 is greedy) and the longest accepted prefix of Eq. 7, plus the bonus
+  token of the all-accepted case (Sec. "Speculative Decoding"); and the
+  greedy walk of a draft tree.
+* ``match`` - the prefix/suffix matcher that resumes Reuse (Sec. "Reuse").
+* ``session`` - prefill / verify / rollback / plain greedy decoding (Eq. 1)
+  over an oracle-owned KV cache.
+"""
+
+from .numerics import round_bf16
+from .model import forward_block, chain_structure, tree_structure
+from .accept import greedy_rows, accept_linear, accept_tree, top2_margin
+from .match import match_reuse
+from .session import OracleSession
+
+__all__ = [
+    "round_bf16", "forward_block", "chain_structure", "tree_structure",
+    "greedy_rows", "accept_linear", "accept_tree", "top2_margin", "match_reuse",
+    "OracleSession",
+]
