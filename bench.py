@@ -1,0 +1,262 @@
+#!/usr/bin/env python
+"""Benchmark of the greedy speculative-verification step on one MI355X.
+
+Workload (synthetic stand-in for the paper's code-editing benchmarks): a
+7B-class Llama-style decoder with random bf16 weights, a 2048-token Zipf
+prompt, and an "original code" c made from the model's own 512-token greedy
+continuation G with 5% of its positions replaced in 3-8-token spans.  Every
+timed step is one Reuse-phase step: the matcher picks where the generated
+output continues in c, K = 32 tokens of c from there are verified in one
+forward, and the accepted prefix plus the target's next token are emitted.
+When G has been re-created in full the sequence is rolled back to the prompt.
+The emitted stream is checked to equal G (greedy verification is lossless).
+
+Printed: one JSON line.  value = emitted tokens per second of the Reuse
+session (the paper's Tokens/s); also the verify-step latency at exactly 2048
+committed positions, the whole-step HBM roofline fraction, the dominant
+kernel's live roofline and the CPU oracle's rate on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verified tokens/sec + verify-step latency at K=32, 7B bf16; % peak HBM BW"
+
+
+def linear_weight_bytes(s) -> int:
+    esz = 2 if s.dtype == "bf16" else 4
+    per_layer = (s.q_dim + 2 * s.kv_dim) * s.d_model + s.d_model * s.q_dim + 3 * s.ffn * s.d_model
+    return esz * (s.n_layers * per_layer + s.vocab * s.d_model)
+
+
+def step_bytes(s, t: int, n: int) -> dict:
+    """Bytes one verify step must move: every weight once, the committed K/V
+    once, the block's K/V written, the gathered embedding rows and the logits."""
+    esz = 2 if s.dtype == "bf16" else 4
+    kv_row = 2 * s.kv_dim * esz * s.n_layers
+    parts = dict(weights=linear_weight_bytes(s), kv_read=n * kv_row, kv_write=t * kv_row,
+                 embed=t * s.d_model * esz, logits=t * s.vocab * 4)
+    parts["total"] = sum(parts.values())
+    return parts
+
+
+def gateup_bytes(s, t: int) -> int:
+    """Algorithmic bytes of one gate/up GEMM launch: the [2F, d] weights, the
+    T normalised input rows and the T SwiGLU output rows."""
+    esz = 2 if s.dtype == "bf16" else 4
+    return esz * (2 * s.ffn * s.d_model + t * s.d_model + t * s.ffn)
+
+
+def cpu_baseline(shape, weights, k: int, ctx: int, layers: int, emitted_per_step: float):
+    """Time the oracle on a bounded sample of one verify step and scale it."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import forward_block, tree_structure  # noqa: F401
+    from oracle.model import chain_structure
+    from oracle.numerics import to_f64
+    from workloads import random_kv_context, zipf_tokens
+
+    class Sub:
+        def __init__(self, w, nl):
+            self.embed, self.lm_head, self.final_gain = w.embed, w.lm_head, w.final_gain
+            self._w, self._nl = w, nl
+
+        def layer(self, l):
+            return self._w.layer(l)
+
+    tokens = zipf_tokens(shape.vocab, k + 1, seed=3)
+    depth, vis = chain_structure(k + 1)
+    kv = random_kv_context(layers, ctx, shape.n_kv_heads, shape.head_dim, seed=5, dtype=shape.dtype)
+    cache = [(to_f64(a, shape.dtype), to_f64(b, shape.dtype)) for a, b in kv]
+
+    def run(nl):
+        sub = shape.with_(n_layers=nl)
+        t0 = time.perf_counter()
+        forward_block(sub, Sub(weights, nl), cache[:nl], tokens, depth, vis)
+        return time.perf_counter() - t0
+
+    t_head = min(run(0) for _ in range(2))
+    t_layers = min(run(layers) for _ in range(2))
+    per_layer = max(t_layers - t_head, 0.0) / layers
+    est = t_head + per_layer * shape.n_layers
+    threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    return {
+        "value": round(emitted_per_step / est, 3), "unit": "tokens/s", "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"one K={k} verify block over a {ctx}-position committed KV cache (random bf16 "
+                   f"values) through {layers} of the {shape.n_layers} layers plus final norm and LM "
+                   f"head, fp64 NumPy; step time = head part + {shape.n_layers}/{layers} x layer part "
+                   f"= {est:.2f} s; tokens/s uses the GPU session's {emitted_per_step:.2f} emitted "
+                   f"tokens per step"),
+        "step_seconds": round(est, 3),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="7b", choices=["tiny", "1b", "7b", "33b"])
+    ap.add_argument("--k", type=int, default=32)
+    ap.add_argument("--ctx", type=int, default=2048)
+    ap.add_argument("--gen", type=int, default=512, help="length of the greedy output re-created")
+    ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the verification step of one edit session is "
+              "not sharded across GPUs in this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2506_02780_amd as ee
+    from workloads import gen_weights, get_shape, inject_edits, zipf_tokens
+
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    shape = get_shape(args.config)
+    K, ctx = args.k, args.ctx
+    t0 = time.perf_counter()
+    weights = gen_weights(shape, seed=1234)
+    log(f"[bench] weights drawn in {time.perf_counter() - t0:.1f}s")
+    max_ctx = ctx + args.gen + K + 2
+    eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=max(K, 1))
+    log(f"[bench] engine ready at {time.perf_counter() - t0:.1f}s")
+
+    prompt = zipf_tokens(shape.vocab, ctx, seed=42)
+    first = eng.prefill(0, prompt)
+    G = [first]
+    for _ in range(args.gen - 1):
+        G.append(eng.verify(0, [])[1])
+    code, _ = inject_edits(np.asarray(G, dtype=np.int32), shape.vocab, seed=7)
+    code = code.tolist()
+    log(f"[bench] prompt + {args.gen}-token greedy output ready at {time.perf_counter() - t0:.1f}s")
+
+    state = {}
+
+    def reset():
+        eng.rollback(0, ctx, first)
+        state.update(gen=[first], cursor=0)
+
+    def reuse_step():
+        gen, cur = state["gen"], state["cursor"]
+        ds, _ = ee.match_reuse(gen, code, cur)
+        start = ds if ds >= 0 else cur
+        d = code[start:start + K]
+        a, nxt, _ = eng.verify(0, d)
+        out = d[:a] + [nxt]
+        n0 = len(gen)
+        gen.extend(out)
+        m = min(len(gen), len(G))
+        if gen[n0:m] != G[n0:m]:
+            raise SystemExit(f"lossless check failed at output position {n0}")
+        state["cursor"] = start + a + 1
+        if len(gen) >= len(G):
+            reset()
+        return len(out)
+
+    reset()
+    for _ in range(args.warmup):
+        reuse_step()
+    eng.profile(["gateup"])
+    eng.profile_read(reset=True)
+    torch.cuda.synchronize()
+    emitted, lat = 0, []
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        ts = time.perf_counter()
+        emitted += reuse_step()
+        lat.append(time.perf_counter() - ts)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    prof = eng.profile_read(reset=True)
+    eng.profile([])
+    gu_ms, gu_n = prof["gateup"]
+    gu_avg_s = gu_ms / 1e3 / gu_n
+    T = K + 1
+    gu_alg = gateup_bytes(shape, T)
+
+    # verify latency at exactly `ctx` committed positions (rollback after every step)
+    fixed = []
+    d = code[1:1 + K]
+    for i in range(60):
+        eng.rollback(0, ctx, first)
+        ts = time.perf_counter()
+        eng.verify(0, d)
+        if i >= 10:
+            fixed.append(time.perf_counter() - ts)
+    p50 = float(np.percentile(fixed, 50))
+    p90 = float(np.percentile(fixed, 90))
+    sb = step_bytes(shape, T, ctx)
+
+    # per-class breakdown of one step (separate pass, every class instrumented)
+    eng.profile(list(ee.PROF_CLASSES))
+    for _ in range(10):
+        eng.rollback(0, ctx, first)
+        eng.verify(0, d)
+    brk = {c: round(ms / 10, 4) for c, (ms, n) in eng.profile_read(reset=True).items() if n}
+    eng.profile([])
+    eng.rollback(0, ctx, first)
+
+    result = {
+        "metric": METRIC,
+        "value": round(emitted / elapsed, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{args.config} Llama-style random-init {shape.dtype}, Reuse session: K={K} "
+                         f"drafts from an edited copy (5% in 3-8-token spans) of the model's own "
+                         f"{args.gen}-token greedy output, after a {ctx}-token Zipf prompt"),
+            "k": K, "prompt_tokens": ctx, "regenerated_tokens": args.gen, "batch": 1,
+        },
+        "emitted_per_step": round(emitted / args.steps, 3),
+        "verify_latency_ms_at_ctx": {"ctx": ctx, "p50": round(p50 * 1e3, 4), "p90": round(p90 * 1e3, 4)},
+        "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
+                     "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4)},
+        "roofline": {
+            "kernel": "gemm_kernel (gate/up projection + SwiGLU epilogue)",
+            "bound": "hbm",
+            "achieved": round(gu_alg / gu_avg_s / 1e9, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gu_alg / gu_avg_s / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "launch_us": round(gu_avg_s * 1e6, 2),
+            "launches": int(gu_n),
+            "bytes_per_launch": gu_alg,
+        },
+        "breakdown_ms_per_step": brk,
+        "lossless_check": "emitted stream equals the GPU's own greedy output",
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample")
+        result["cpu_baseline"] = cpu_baseline(shape, weights, K, ctx, args.cpu_layers,
+                                              emitted / args.steps)
+    eng.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

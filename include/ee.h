@@ -1,0 +1,196 @@
+/*
+ * ee.h - C ABI of the MI355X greedy speculative-verification library.
+ *
+ * The library runs the target-model side of edit-oriented speculative
+ * decoding on one gfx950 GPU: a decoder-only transformer forward over a block
+ * of draft tokens appended to a paged KV cache (Eq. 3), greedy decoding of
+ * every row, the longest accepted draft prefix (Eq. 7, Sec. "Reuse"), and the
+ * KV-cache commit/rollback that keeps only the accepted rows.  The Reuse
+ * phase's draft source - the prefix/suffix matcher between generated tokens
+ * and the original code (Sec. "Reuse") - is exported too (host code).
+ *
+ * Conventions shared by every call
+ *  - Device memory is owned by the caller: weights, the packed-weight arena,
+ *    the KV pool and the workspace are caller allocations whose device
+ *    pointers are handed over at ee_create and must stay valid until
+ *    ee_destroy.  The library never frees them and allocates no device memory
+ *    of its own (it allocates small pinned host staging buffers).
+ *  - Host arrays passed to a call are read during the call only; host outputs
+ *    are written before the call returns.  ee_prefill and ee_verify are
+ *    synchronous: they return after the GPU work of the call has finished.
+ *  - Every call validates all of its arguments before it launches anything;
+ *    a call that fails leaves the sequence state (committed length, pending
+ *    token, KV contents) unchanged.  No C++ exception crosses the boundary.
+ *  - Return codes: EE_OK (0) or a negative EE_E* value; ee_last_error gives a
+ *    message for the last failure on a context.
+ *  - A context is not thread-safe; calls on one context must not overlap.
+ */
+#ifndef EE_H
+#define EE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  EE_OK = 0,
+  EE_EINVAL = -1,     /* bad argument (shape, range, NULL, malformed tree)   */
+  EE_ECAPACITY = -2,  /* KV pool, max_ctx, max_seqs or k_max exceeded         */
+  EE_ESTATE = -3,     /* e.g. verify before prefill, rollback beyond length   */
+  EE_EHIP = -4        /* a HIP runtime call failed                            */
+};
+
+enum { EE_F32 = 0, EE_BF16 = 1 };
+
+typedef struct ee_ctx ee_ctx;
+
+/* Shape of a Llama-style decoder (RMSNorm, rotary positions with rotate-half
+ * pairs, grouped-query attention with contiguous head groups, SwiGLU FFN, no
+ * biases, untied LM head).  Requirements checked by ee_create:
+ *   head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ *   d_model, ffn, n_heads*head_dim and vocab multiples of 32 (bf16) or 16 (f32);
+ *   page_size == 64; 0 <= k_max <= 64; max_ctx >= 1; max_seqs >= 1.       */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t dtype;        /* EE_F32 or EE_BF16: weights, KV cache, GEMM inputs */
+  float rms_eps;        /* RMSNorm epsilon                                   */
+  float rope_theta;     /* rotary base                                        */
+  int32_t max_ctx;      /* longest sequence (committed + one block)          */
+  int32_t max_seqs;     /* sequences that may be live at once                */
+  int32_t k_max;        /* largest draft (linear length or tree node count)  */
+  int32_t page_size;    /* KV positions per page                              */
+} ee_model_config;
+
+/* Logical weights, device pointers, row-major [out, in] in the model dtype.
+ * Per-layer entries are host arrays of n_layers device pointers.  They are
+ * read only inside ee_create (packed into the arena) and may be freed after. */
+typedef struct {
+  const void* embed;                 /* [vocab, d_model]                     */
+  const void* lm_head;               /* [vocab, d_model]                     */
+  const float* final_gain;           /* [d_model] fp32                       */
+  const void* const* wq;             /* [n_heads*head_dim, d_model]          */
+  const void* const* wk;             /* [n_kv_heads*head_dim, d_model]       */
+  const void* const* wv;             /* [n_kv_heads*head_dim, d_model]       */
+  const void* const* wo;             /* [d_model, n_heads*head_dim]          */
+  const void* const* w_gate;         /* [ffn, d_model]                       */
+  const void* const* w_up;           /* [ffn, d_model]                       */
+  const void* const* w_down;         /* [d_model, ffn]                       */
+  const float* const* attn_gain;     /* [d_model] fp32, attention-side norm  */
+  const float* const* ffn_gain;      /* [d_model] fp32, FFN-side norm        */
+} ee_weights;
+
+/* Sizes of the three caller allocations (bytes, 256-byte aligned pieces).
+ * Return 0 for an invalid config. */
+size_t ee_packed_weight_bytes(const ee_model_config* cfg);
+size_t ee_kv_pool_bytes(const ee_model_config* cfg);
+size_t ee_workspace_bytes(const ee_model_config* cfg);
+
+/* Build a context.  Packs every weight into `packed` (the library's
+ * MFMA-fragment layout) and zeroes `kv_pool`, on `hip_stream` (a hipStream_t;
+ * NULL = the default stream), then synchronizes that stream.  All later GPU
+ * work of the context runs on the same stream. */
+int32_t ee_create(const ee_model_config* cfg, const ee_weights* w, void* packed,
+                  void* kv_pool, void* workspace, void* hip_stream, ee_ctx** out);
+int32_t ee_destroy(ee_ctx* ctx);
+
+/* Run the prompt tokens[0..n-1] of sequence `seq` (which must be empty) in
+ * blocks of at most k_max+1 rows, commit all n positions to the KV cache and
+ * return the greedy token of the last row in *next_token: the first emitted
+ * token, now "pending" (emitted, not yet run through the model).  n >= 1.   */
+int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
+                   int32_t* next_token);
+
+/* One verification step (Eq. 3 forward + Eq. 7 acceptance).  The block is
+ * [pending, d_1..d_K]: row 0 is the pending token at position len; draft row
+ * i sits at position len + depth(i).  Every row is decoded greedily (argmax
+ * over the vocabulary, lowest index on exact ties).
+ *   parent == NULL: linear chain; accept_len = largest a with d_i equal to
+ *     the greedy token of row i-1 for all i <= a; next_token = greedy token of
+ *     row a (the correction after a rejection, the bonus token if a == K).
+ *   parent != NULL: draft tree of K nodes; parent[i] is the node that node i
+ *     extends (-1 = the pending token) and must satisfy parent[i] < i; node i
+ *     sees the committed cache, the pending row and its ancestors.  Greedy
+ *     walk: from the pending row, step to the lowest-indexed child whose token
+ *     equals the current row's greedy token.  accept_len = nodes on that path,
+ *     next_token = greedy token of the last one; accepted_nodes (optional,
+ *     room for K entries) receives the path's node indices in depth order.
+ * Effects: the pending row and the accepted rows are committed (len grows by
+ * 1 + accept_len, tree rows compacted to depth order), next_token becomes
+ * pending.  K = 0 is exactly one plain greedy decoding step (Eq. 1).
+ * Errors: EE_ESTATE before prefill; EE_EINVAL for K < 0, K > k_max, a token
+ * outside [0, vocab) or a malformed tree; EE_ECAPACITY if len + K + 1 would
+ * exceed max_ctx or the KV pool has no free page. */
+int32_t ee_verify(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t K,
+                  const int32_t* parent, int32_t* accept_len, int32_t* next_token,
+                  int32_t* accepted_nodes);
+
+/* Truncate sequence `seq` to its first new_len committed positions
+ * (new_len <= len), release pages wholly beyond them and make pending_token
+ * pending.  new_len == 0 with pending_token == -1 empties the sequence (it
+ * may then be prefilled again).  EE_ESTATE if new_len > len. */
+int32_t ee_kv_rollback(ee_ctx* ctx, int32_t seq, int32_t new_len, int32_t pending_token);
+
+/* Committed length and pending token of a sequence (pending -1 if empty). */
+int32_t ee_seq_state(ee_ctx* ctx, int32_t seq, int32_t* len, int32_t* pending_token);
+
+/* Reuse-phase matcher (Sec. "Reuse"; host only, no context needed).  Tries
+ * suffix lengths L from min(max_ngram, n_gen) down to min_ngram; for the first
+ * L that matches, returns the smallest j with original[j..j+L) equal to the
+ * last L generated tokens, j + L >= cursor (the draft starts in the remaining
+ * original code) and j + L < n_orig (a non-empty draft): *draft_start = j + L,
+ * *match_len = L.  No match: *draft_start = -1, *match_len = 0 (EE_OK).
+ * EE_EINVAL for NULL outputs, negative sizes or min_ngram < 1. */
+int32_t ee_match_reuse(const int32_t* generated, int32_t n_gen, const int32_t* original,
+                       int32_t n_orig, int32_t cursor, int32_t min_ngram, int32_t max_ngram,
+                       int32_t* draft_start, int32_t* match_len);
+
+/* Copy the logits of the last prefill block or verify block (rows x vocab,
+ * fp32, row-major) to host memory; rows must equal that block's row count.
+ * Test and inspection aid; not needed on the hot path. */
+int32_t ee_get_logits(ee_ctx* ctx, float* host_out, int32_t rows);
+
+/* Copy committed keys/values of one layer to host memory, positions
+ * [0, len) of sequence `seq`, as [len, n_kv_heads, head_dim] in the model
+ * dtype (fp32 or bf16 bits).  Either output may be NULL.  Test aid. */
+int32_t ee_read_kv(ee_ctx* ctx, int32_t seq, int32_t layer, void* host_k, void* host_v);
+
+/* Kernel classes of one forward, for ee_profile. */
+enum {
+  EE_PROF_NORM = 0,     /* embedding gather + RMSNorm launches          */
+  EE_PROF_QKV = 1,      /* QKV GEMM + rotary + KV append                */
+  EE_PROF_ATTN = 2,     /* split attention over the paged KV cache      */
+  EE_PROF_COMBINE = 3,  /* merge of the attention splits                */
+  EE_PROF_OPROJ = 4,    /* O-projection GEMM + residual                 */
+  EE_PROF_GATEUP = 5,   /* gate/up GEMM + SwiGLU                        */
+  EE_PROF_DOWN = 6,     /* down-projection GEMM + residual              */
+  EE_PROF_LMHEAD = 7,   /* LM-head GEMM + per-tile argmax partials      */
+  EE_PROF_ARGMAX = 8,   /* vocabulary argmax                            */
+  EE_PROF_ACCEPT = 9,   /* acceptance scan / tree walk                  */
+  EE_PROF_COMPACT = 10, /* tree KV compaction                           */
+  EE_PROF_N = 11
+};
+
+/* Measurement aid: when bit c of class_mask is set, every launch of kernel
+ * class c is bracketed by two HIP events on the context's stream, and the
+ * elapsed time between them is accumulated after each prefill / verify
+ * block.  class_mask = 0 turns it off (the default).  The events add a small
+ * overhead to the instrumented launches only. */
+int32_t ee_profile(ee_ctx* ctx, uint32_t class_mask);
+
+/* Read the accumulated per-class totals: ms[EE_PROF_N] milliseconds and
+ * launches[EE_PROF_N] launch counts (either may be NULL); reset != 0 zeroes
+ * them afterwards. */
+int32_t ee_profile_read(ee_ctx* ctx, double* ms, int64_t* launches, int32_t reset);
+
+/* Message for the last failed call on ctx (or the last failed context-free
+ * call when ctx is NULL).  Never NULL; the pointer stays valid until the next
+ * call on the same context. */
+const char* ee_last_error(const ee_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EE_H */

@@ -1,0 +1,239 @@
+"""Python binding of the MI355X greedy speculative-verification library.
+
+A thin ctypes layer over the C ABI of ``include/ee.h``: it allocates device
+memory with PyTorch (weights, packed-weight arena, KV pool, workspace),
+passes raw pointers and the current HIP stream, and converts arguments and
+results.  Every step of the verification path runs in the HIP kernels of
+``libee.so``; nothing here computes any part of it.  If the library has not
+been built, importing this package raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loaded first so the HIP runtime it ships is the one libee.so binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libee.so")
+
+EE_OK, EE_EINVAL, EE_ECAPACITY, EE_ESTATE, EE_EHIP = 0, -1, -2, -3, -4
+EE_F32, EE_BF16 = 0, 1
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_i32, _vp, _sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+_pi32 = ctypes.POINTER(ctypes.c_int32)
+
+
+class EEModelConfig(ctypes.Structure):
+    _fields_ = [("n_layers", _i32), ("d_model", _i32), ("n_heads", _i32), ("n_kv_heads", _i32),
+                ("head_dim", _i32), ("ffn", _i32), ("vocab", _i32), ("dtype", _i32),
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("max_ctx", _i32), ("max_seqs", _i32), ("k_max", _i32), ("page_size", _i32)]
+
+
+class EEWeights(ctypes.Structure):
+    _fields_ = [("embed", _vp), ("lm_head", _vp), ("final_gain", _vp),
+                ("wq", ctypes.POINTER(_vp)), ("wk", ctypes.POINTER(_vp)), ("wv", ctypes.POINTER(_vp)),
+                ("wo", ctypes.POINTER(_vp)), ("w_gate", ctypes.POINTER(_vp)),
+                ("w_up", ctypes.POINTER(_vp)), ("w_down", ctypes.POINTER(_vp)),
+                ("attn_gain", ctypes.POINTER(_vp)), ("ffn_gain", ctypes.POINTER(_vp))]
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype, f.argtypes = res, args
+    return f
+
+
+ee_packed_weight_bytes = _sig("ee_packed_weight_bytes", _sz, [ctypes.POINTER(EEModelConfig)])
+ee_kv_pool_bytes = _sig("ee_kv_pool_bytes", _sz, [ctypes.POINTER(EEModelConfig)])
+ee_workspace_bytes = _sig("ee_workspace_bytes", _sz, [ctypes.POINTER(EEModelConfig)])
+ee_create = _sig("ee_create", _i32, [ctypes.POINTER(EEModelConfig), ctypes.POINTER(EEWeights),
+                                     _vp, _vp, _vp, _vp, ctypes.POINTER(_vp)])
+ee_destroy = _sig("ee_destroy", _i32, [_vp])
+ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
+ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
+ee_kv_rollback = _sig("ee_kv_rollback", _i32, [_vp, _i32, _i32, _i32])
+ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
+ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32, _i32, _i32, _pi32, _pi32])
+ee_get_logits = _sig("ee_get_logits", _i32, [_vp, ctypes.POINTER(ctypes.c_float), _i32])
+ee_read_kv = _sig("ee_read_kv", _i32, [_vp, _i32, _i32, _vp, _vp])
+ee_last_error = _sig("ee_last_error", ctypes.c_char_p, [_vp])
+ee_profile = _sig("ee_profile", _i32, [_vp, ctypes.c_uint32])
+ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_double),
+                                                 ctypes.POINTER(ctypes.c_int64), _i32])
+
+PROF_CLASSES = ("norm", "qkv", "attn", "combine", "oproj", "gateup", "down", "lmhead", "argmax",
+                "accept", "compact")
+
+
+class EEError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"ee error {code}: {msg}")
+        self.code = code
+
+
+def _check(rc: int, ctx=None):
+    if rc != EE_OK:
+        raise EEError(rc, ee_last_error(ctx).decode())
+
+
+def _i32arr(x):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+    return a, a.ctypes.data_as(_pi32)
+
+
+def make_config(shape, max_ctx: int, max_seqs: int = 1, k_max: int = 64) -> EEModelConfig:
+    return EEModelConfig(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads,
+                         shape.head_dim, shape.ffn, shape.vocab,
+                         EE_BF16 if shape.dtype == "bf16" else EE_F32,
+                         shape.rms_eps, shape.rope_theta, max_ctx, max_seqs, k_max, 64)
+
+
+def match_reuse(generated, original, cursor: int, min_ngram: int = 1, max_ngram: int = 8):
+    """Reuse-phase matcher: (draft_start, match_len), (-1, 0) if nothing matches."""
+    g, gp = _i32arr(generated)
+    o, op = _i32arr(original)
+    ds, ml = ctypes.c_int32(), ctypes.c_int32()
+    _check(ee_match_reuse_c(gp, len(g), op, len(o), cursor, min_ngram, max_ngram,
+                            ctypes.byref(ds), ctypes.byref(ml)))
+    return ds.value, ml.value
+
+
+def _to_device(a: np.ndarray, device) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16))
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(device, non_blocking=False)
+
+
+class Engine:
+    """One library context: packed weights, a paged KV pool, one workspace.
+
+    ``weights`` provides numpy arrays in the model dtype (``embed``,
+    ``lm_head``, ``final_gain``, ``layer(l)`` mapping), as drawn by
+    ``workloads.gen_weights``.
+    """
+
+    def __init__(self, shape, weights, max_ctx: int, max_seqs: int = 1, k_max: int = 64,
+                 device: str = "cuda:0"):
+        if not torch.cuda.is_available():
+            raise RuntimeError("the verification library needs a ROCm GPU")
+        self.shape, self.device = shape, torch.device(device)
+        self.cfg = make_config(shape, max_ctx, max_seqs, k_max)
+        cfgp = ctypes.byref(self.cfg)
+        nb_packed, nb_kv, nb_ws = ee_packed_weight_bytes(cfgp), ee_kv_pool_bytes(cfgp), ee_workspace_bytes(cfgp)
+        if not (nb_packed and nb_kv and nb_ws):
+            raise EEError(EE_EINVAL, "invalid model config for the library")
+        with torch.cuda.device(self.device):
+            self.packed = torch.empty(nb_packed, dtype=torch.uint8, device=self.device)
+            self.kv_pool = torch.empty(nb_kv, dtype=torch.uint8, device=self.device)
+            self.workspace = torch.empty(nb_ws, dtype=torch.uint8, device=self.device)
+            self.stream = torch.cuda.current_stream(self.device)
+            keep = []
+
+            def dev(a):
+                t = _to_device(a, self.device)
+                keep.append(t)
+                return t.data_ptr()
+
+            L = shape.n_layers
+            arr = lambda: (_vp * L)()
+            ptrs = {k: arr() for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
+                                       "attn_gain", "ffn_gain")}
+            for l in range(L):
+                lw = weights.layer(l)
+                for k in ptrs:
+                    ptrs[k][l] = dev(lw[k])
+            w = EEWeights(dev(weights.embed), dev(weights.lm_head), dev(weights.final_gain),
+                          *[ctypes.cast(ptrs[k], ctypes.POINTER(_vp)) for k in
+                            ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "attn_gain", "ffn_gain")])
+            torch.cuda.synchronize(self.device)
+            ctx = _vp()
+            _check(ee_create(cfgp, ctypes.byref(w), self.packed.data_ptr(), self.kv_pool.data_ptr(),
+                             self.workspace.data_ptr(), self.stream.cuda_stream, ctypes.byref(ctx)))
+            self.ctx = ctx
+            del keep
+        self._last_rows = 0
+
+    # -- calls ---------------------------------------------------------------
+    def prefill(self, seq: int, tokens) -> int:
+        t, tp = _i32arr(tokens)
+        nxt = ctypes.c_int32()
+        _check(ee_prefill(self.ctx, seq, tp, len(t), ctypes.byref(nxt)), self.ctx)
+        self._last_rows = min(len(t) - (len(t) - 1) // (self.cfg.k_max + 1) * (self.cfg.k_max + 1),
+                              self.cfg.k_max + 1)
+        return nxt.value
+
+    def verify(self, seq: int, draft, parent=None):
+        """Returns (accept_len, next_token, accepted_nodes or None)."""
+        d, dp = _i32arr(draft)
+        k = len(d)
+        a, nxt = ctypes.c_int32(), ctypes.c_int32()
+        if parent is not None:
+            p, pp = _i32arr(parent)
+            if len(p) != k:
+                raise EEError(EE_EINVAL, "parent must have one entry per draft node")
+            nodes = np.zeros(max(k, 1), dtype=np.int32)
+            _check(ee_verify(self.ctx, seq, dp, k, pp, ctypes.byref(a), ctypes.byref(nxt),
+                             nodes.ctypes.data_as(_pi32)), self.ctx)
+            self._last_rows = k + 1
+            return a.value, nxt.value, nodes[:a.value].copy()
+        _check(ee_verify(self.ctx, seq, dp, k, None, ctypes.byref(a), ctypes.byref(nxt), None), self.ctx)
+        self._last_rows = k + 1
+        return a.value, nxt.value, None
+
+    def rollback(self, seq: int, new_len: int, pending: int):
+        _check(ee_kv_rollback(self.ctx, seq, new_len, pending), self.ctx)
+
+    def seq_state(self, seq: int):
+        n, p = ctypes.c_int32(), ctypes.c_int32()
+        _check(ee_seq_state(self.ctx, seq, ctypes.byref(n), ctypes.byref(p)), self.ctx)
+        return n.value, p.value
+
+    def logits(self) -> np.ndarray:
+        rows = self._last_rows
+        out = np.empty((rows, self.shape.vocab), dtype=np.float32)
+        _check(ee_get_logits(self.ctx, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), rows), self.ctx)
+        return out
+
+    def read_kv(self, seq: int, layer: int):
+        n, _ = self.seq_state(seq)
+        s = self.shape
+        dt = np.uint16 if s.dtype == "bf16" else np.float32
+        k = np.empty((n, s.n_kv_heads, s.head_dim), dtype=dt)
+        v = np.empty_like(k)
+        _check(ee_read_kv(self.ctx, seq, layer, k.ctypes.data, v.ctypes.data), self.ctx)
+        return k, v
+
+    def profile(self, classes=()):
+        """Bracket launches of the named kernel classes with HIP events."""
+        mask = 0
+        for c in classes:
+            mask |= 1 << PROF_CLASSES.index(c)
+        _check(ee_profile(self.ctx, mask), self.ctx)
+
+    def profile_read(self, reset: bool = True):
+        """{class: (total ms, launches)} accumulated since the last reset."""
+        ms = (ctypes.c_double * len(PROF_CLASSES))()
+        n = (ctypes.c_int64 * len(PROF_CLASSES))()
+        _check(ee_profile_read(self.ctx, ms, n, int(reset)), self.ctx)
+        return {c: (ms[i], n[i]) for i, c in enumerate(PROF_CLASSES)}
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            _check(ee_destroy(self.ctx))
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,592 @@
+// Host engine behind the C ABI of include/ee.h: argument validation, the
+// paged KV allocator, per-sequence state, host<->device staging and the
+// launch sequence of one verification step.
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/ee.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int PAGE = 64;
+constexpr int SPLIT = 256;
+constexpr size_t ALIGN = 256;
+
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+thread_local std::string g_err = "no error";
+
+struct Seq {
+  bool live = false;
+  int len = 0;
+  int pending = -1;
+  std::vector<int> pages;   // page of positions [64 i, 64 i + 64)
+};
+
+// Byte offsets of every buffer inside the three caller allocations.
+struct Layout {
+  int Tmax, MT, G, max_splits, pages_per_seq, n_pages;
+  // packed arena
+  size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
+      packed_total;
+  // workspace
+  size_t h, xbuf, zbuf, q, part, logits, amax, greedy, result, stage, rope, ws_total;
+  // staging sub-offsets (relative to `stage`)
+  size_t s_tok, s_pos, s_prow, s_anc, s_ptable, stage_bytes;
+  size_t kv_layer, kv_total;
+};
+
+bool valid_cfg(const ee_model_config* c, std::string* why) {
+  auto bad = [&](const char* m) { if (why) *why = m; return false; };
+  if (!c) return bad("config is NULL");
+  if (c->dtype != EE_F32 && c->dtype != EE_BF16) return bad("dtype must be EE_F32 or EE_BF16");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->n_kv_heads < 1 || c->ffn < 1 ||
+      c->vocab < 1)
+    return bad("every model dimension must be positive");
+  if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c->n_heads % c->n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
+  const int ks = c->dtype == EE_BF16 ? 32 : 16;
+  if (c->d_model % ks || c->ffn % ks || (c->n_heads * c->head_dim) % ks || c->vocab % ks)
+    return bad("d_model, ffn, n_heads*head_dim and vocab must be multiples of 32 (bf16) / 16 (f32)");
+  if (c->page_size != PAGE) return bad("page_size must be 64");
+  if (c->k_max < 0 || c->k_max > 64) return bad("k_max must be in [0, 64]");
+  if (c->max_ctx < 1 || c->max_seqs < 1) return bad("max_ctx and max_seqs must be positive");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0");
+  if ((c->n_heads / c->n_kv_heads) * (c->k_max + 1) > 64 * 16 * 16)
+    return bad("too many query columns per KV head");
+  return true;
+}
+
+Layout make_layout(const ee_model_config* c) {
+  Layout L{};
+  const size_t esz = c->dtype == EE_BF16 ? 2 : 4;
+  const int ks = c->dtype == EE_BF16 ? 32 : 16;
+  const size_t d = c->d_model, hd = c->head_dim, H = c->n_heads, Hkv = c->n_kv_heads;
+  const size_t F = c->ffn, V = c->vocab;
+  L.Tmax = c->k_max + 1;
+  L.MT = (L.Tmax + 15) / 16;
+  L.G = c->n_heads / c->n_kv_heads;
+  L.max_splits = (c->max_ctx + SPLIT - 1) / SPLIT + 1;
+  L.pages_per_seq = (c->max_ctx + PAGE - 1) / PAGE;
+  L.n_pages = L.pages_per_seq * c->max_seqs;
+  // packed arena
+  size_t o = 0;
+  L.embed = o; o += up(V * d * esz);
+  L.lm_head = o; o += up(V * d * esz);
+  L.final_gain = o; o += up(d * 4);
+  L.layers0 = o;
+  L.l_wqkv = 0;
+  size_t lo = 0;
+  lo += up((H + 2 * Hkv) * hd * d * esz); L.l_wo = lo;
+  lo += up(d * H * hd * esz); L.l_wgu = lo;
+  lo += up(2 * F * d * esz); L.l_wd = lo;
+  lo += up(d * F * esz); L.l_again = lo;
+  lo += up(d * 4); L.l_fgain = lo;
+  lo += up(d * 4);
+  L.per_layer = lo;
+  L.packed_total = o + lo * c->n_layers;
+  // workspace
+  const size_t Tpad = (size_t)L.MT * 16;
+  const size_t xcols = std::max(d, H * hd);
+  o = 0;
+  L.h = o; o += up(L.Tmax * d * 4);
+  L.xbuf = o; o += up(Tpad * xcols * esz);
+  L.zbuf = o; o += up(Tpad * F * esz);
+  L.q = o; o += up(L.Tmax * H * hd * esz);
+  L.part = o; o += up((size_t)L.max_splits * Hkv * L.Tmax * L.G * (hd + 2) * 4);
+  L.logits = o; o += up(L.Tmax * V * 4);
+  L.amax = o; o += up(L.Tmax * (V / 16) * 8);
+  L.greedy = o; o += up(L.Tmax * 4);
+  L.result = o; o += up((2 + 64) * 4);
+  // staging block: one host->device copy per call
+  size_t so = 0;
+  L.s_anc = so; so += L.Tmax * 8;
+  L.s_tok = so; so += L.Tmax * 4;
+  L.s_pos = so; so += L.Tmax * 4;
+  L.s_prow = so; so += L.Tmax * 4;
+  L.s_ptable = so; so += L.pages_per_seq * 4;
+  L.stage_bytes = up(so);
+  L.stage = o; o += L.stage_bytes;
+  L.rope = o; o += up((size_t)c->max_ctx * (hd / 2) * 8);
+  L.ws_total = o;
+  (void)ks;
+  // KV pool: [layer][page][2][Hkv][64 * hd]
+  L.kv_layer = (size_t)L.n_pages * 2 * Hkv * PAGE * hd * esz;
+  L.kv_total = L.kv_layer * c->n_layers;
+  return L;
+}
+
+}  // namespace
+
+struct ee_ctx {
+  ee_model_config cfg;
+  Layout lay;
+  hipStream_t st = nullptr;
+  unsigned char* packed = nullptr;
+  unsigned char* pool = nullptr;
+  unsigned char* ws = nullptr;
+  std::vector<ee::LayerPtrs> layers;
+  ee::Model m{};
+  ee::Work w{};
+  std::vector<Seq> seqs;
+  std::vector<int> free_pages;
+  unsigned char* h_stage = nullptr;   // pinned mirror of the staging block
+  int* h_result = nullptr;            // pinned
+  int last_T = 0;
+  std::string err = "no error";
+  // profiling
+  ee::Prof prof;
+  std::vector<hipEvent_t> events;
+  std::vector<int> ev_cls;
+  double prof_ms[ee::PC_N] = {};
+  int64_t prof_n[ee::PC_N] = {};
+};
+
+namespace {
+
+int fail(ee_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg; else g_err = msg;
+  return code;
+}
+
+int hip_fail(ee_ctx* c, hipError_t e, const char* where) {
+  return fail(c, EE_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, expr)                                      \
+  do {                                                          \
+    hipError_t e_ = (expr);                                     \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);    \
+  } while (0)
+
+void bind_work(ee_ctx* c) {
+  const Layout& L = c->lay;
+  unsigned char* ws = c->ws;
+  ee::Work& w = c->w;
+  w.h = reinterpret_cast<float*>(ws + L.h);
+  w.xbuf = reinterpret_cast<uint4*>(ws + L.xbuf);
+  w.zbuf = reinterpret_cast<uint4*>(ws + L.zbuf);
+  w.q = ws + L.q;
+  w.attn_part = reinterpret_cast<float*>(ws + L.part);
+  w.logits = reinterpret_cast<float*>(ws + L.logits);
+  w.amax = reinterpret_cast<unsigned long long*>(ws + L.amax);
+  w.greedy = reinterpret_cast<int*>(ws + L.greedy);
+  w.result = reinterpret_cast<int*>(ws + L.result);
+  unsigned char* sb = ws + L.stage;
+  w.anc = reinterpret_cast<unsigned long long*>(sb + L.s_anc);
+  w.tok = reinterpret_cast<int*>(sb + L.s_tok);
+  w.pos = reinterpret_cast<int*>(sb + L.s_pos);
+  w.prow = reinterpret_cast<int*>(sb + L.s_prow);
+  w.ptable = reinterpret_cast<int*>(sb + L.s_ptable);
+  w.max_splits = L.max_splits;
+}
+
+// Give `s` pages for positions [0, upto); returns false (and takes nothing)
+// when the pool runs dry.
+bool reserve_pages(ee_ctx* c, Seq& s, int upto, int* added) {
+  const int need = (upto + PAGE - 1) / PAGE;
+  const int have = (int)s.pages.size();
+  *added = 0;
+  if (need <= have) return true;
+  if ((int)c->free_pages.size() < need - have) return false;
+  for (int i = have; i < need; ++i) {
+    s.pages.push_back(c->free_pages.back());
+    c->free_pages.pop_back();
+  }
+  *added = need - have;
+  return true;
+}
+
+void unreserve(ee_ctx* c, Seq& s, int n) {
+  for (int i = 0; i < n; ++i) {
+    c->free_pages.push_back(s.pages.back());
+    s.pages.pop_back();
+  }
+}
+
+int check_seq(ee_ctx* c, int seq) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (seq < 0 || seq >= c->cfg.max_seqs) return fail(c, EE_EINVAL, "sequence index out of range");
+  return EE_OK;
+}
+
+// Stage rows, run the forward + acceptance (+ tree compaction), fetch the
+// result.  Returns EE_OK and fills h_result.
+int run_block(ee_ctx* c, Seq& s, int T, int mode) {
+  const Layout& L = c->lay;
+  int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
+  for (size_t i = 0; i < s.pages.size(); ++i) ptab[i] = s.pages[i];
+  HIP_TRY(c, hipMemcpyAsync(c->ws + L.stage, c->h_stage, L.stage_bytes, hipMemcpyHostToDevice, c->st));
+  ee::Step step{T, s.len, mode};
+  ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
+  c->prof.used = 0;
+  HIP_TRY(c, ee::run_forward(c->m, c->w, step, prof, c->st));
+  HIP_TRY(c, ee::run_accept(c->m, c->w, step, prof, c->st));
+  if (mode == 2) HIP_TRY(c, ee::run_compact(c->m, c->w, step, prof, c->st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (2 + 64) * sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(c, hipStreamSynchronize(c->st));
+  for (int i = 0; prof && i < c->prof.used; ++i) {
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, c->events[2 * i], c->events[2 * i + 1]));
+    c->prof_ms[c->ev_cls[i]] += ms;
+    c->prof_n[c->ev_cls[i]] += 1;
+  }
+  c->last_T = T;
+  return EE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ee_packed_weight_bytes(const ee_model_config* cfg) {
+  if (!valid_cfg(cfg, nullptr)) return 0;
+  return make_layout(cfg).packed_total;
+}
+
+size_t ee_kv_pool_bytes(const ee_model_config* cfg) {
+  if (!valid_cfg(cfg, nullptr)) return 0;
+  return make_layout(cfg).kv_total;
+}
+
+size_t ee_workspace_bytes(const ee_model_config* cfg) {
+  if (!valid_cfg(cfg, nullptr)) return 0;
+  return make_layout(cfg).ws_total;
+}
+
+int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packed, void* kv_pool,
+                  void* workspace, void* hip_stream, ee_ctx** out) {
+  std::string why;
+  if (!out) return fail(nullptr, EE_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!valid_cfg(cfg, &why)) return fail(nullptr, EE_EINVAL, why);
+  if (!wts || !packed || !kv_pool || !workspace)
+    return fail(nullptr, EE_EINVAL, "weights, packed arena, KV pool and workspace must be non-NULL");
+  const int nl = cfg->n_layers;
+  if (!wts->embed || !wts->lm_head || !wts->final_gain || !wts->wq || !wts->wk || !wts->wv ||
+      !wts->wo || !wts->w_gate || !wts->w_up || !wts->w_down || !wts->attn_gain || !wts->ffn_gain)
+    return fail(nullptr, EE_EINVAL, "a weight pointer is NULL");
+  for (int l = 0; l < nl; ++l)
+    if (!wts->wq[l] || !wts->wk[l] || !wts->wv[l] || !wts->wo[l] || !wts->w_gate[l] ||
+        !wts->w_up[l] || !wts->w_down[l] || !wts->attn_gain[l] || !wts->ffn_gain[l])
+      return fail(nullptr, EE_EINVAL, "a per-layer weight pointer is NULL");
+
+  ee_ctx* c = new (std::nothrow) ee_ctx();
+  if (!c) return fail(nullptr, EE_EINVAL, "out of host memory");
+  c->cfg = *cfg;
+  c->lay = make_layout(cfg);
+  c->st = reinterpret_cast<hipStream_t>(hip_stream);
+  c->packed = reinterpret_cast<unsigned char*>(packed);
+  c->pool = reinterpret_cast<unsigned char*>(kv_pool);
+  c->ws = reinterpret_cast<unsigned char*>(workspace);
+  const Layout& L = c->lay;
+  const int dt = cfg->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
+  const size_t esz = ee::esz_of(dt);
+  const int d = cfg->d_model, hd = cfg->head_dim, H = cfg->n_heads, Hkv = cfg->n_kv_heads, F = cfg->ffn;
+
+  auto cleanup = [&](int code) {
+    if (c->h_stage) (void)hipHostFree(c->h_stage);
+    if (c->h_result) (void)hipHostFree(c->h_result);
+    g_err = c->err;
+    delete c;
+    return code;
+  };
+  hipError_t e;
+  if ((e = hipHostMalloc(reinterpret_cast<void**>(&c->h_stage), L.stage_bytes, hipHostMallocDefault)) != hipSuccess ||
+      (e = hipHostMalloc(reinterpret_cast<void**>(&c->h_result), (2 + 64) * sizeof(int), hipHostMallocDefault)) != hipSuccess) {
+    hip_fail(c, e, "hipHostMalloc");
+    return cleanup(EE_EHIP);
+  }
+  memset(c->h_stage, 0, L.stage_bytes);
+
+  // pack weights
+  auto run = [&](hipError_t err, const char* where) {
+    if (err != hipSuccess) { hip_fail(c, err, where); return false; }
+    return true;
+  };
+  bool ok = run(ee::launch_copy(wts->embed, c->packed + L.embed, (size_t)cfg->vocab * d * esz, c->st), "copy embed") &&
+            run(ee::launch_copy(wts->final_gain, c->packed + L.final_gain, (size_t)d * 4, c->st), "copy gain");
+  ee::PackSrc ps{};
+  ps.src0 = wts->lm_head; ps.rows = cfg->vocab; ps.map = ee::ROWS_IDENTITY; ps.dst_row0 = 0;
+  ok = ok && run(ee::launch_pack(ps, c->packed + L.lm_head, d, dt, hd, c->st), "pack lm_head");
+  c->layers.resize(nl);
+  for (int l = 0; l < nl && ok; ++l) {
+    unsigned char* lb = c->packed + L.layers0 + (size_t)l * L.per_layer;
+    ee::LayerPtrs& lp = c->layers[l];
+    lp.wqkv = reinterpret_cast<const uint4*>(lb + L.l_wqkv);
+    lp.wo = reinterpret_cast<const uint4*>(lb + L.l_wo);
+    lp.wgu = reinterpret_cast<const uint4*>(lb + L.l_wgu);
+    lp.wd = reinterpret_cast<const uint4*>(lb + L.l_wd);
+    lp.attn_gain = reinterpret_cast<const float*>(lb + L.l_again);
+    lp.ffn_gain = reinterpret_cast<const float*>(lb + L.l_fgain);
+    ee::PackSrc p{};
+    p = {wts->wq[l], nullptr, H * hd, ee::ROWS_ROPE, 0};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wq");
+    p = {wts->wk[l], nullptr, Hkv * hd, ee::ROWS_ROPE, H * hd};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wk");
+    p = {wts->wv[l], nullptr, Hkv * hd, ee::ROWS_IDENTITY, (H + Hkv) * hd};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wv");
+    p = {wts->wo[l], nullptr, d, ee::ROWS_IDENTITY, 0};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wo, H * hd, dt, hd, c->st), "pack wo");
+    p = {wts->w_gate[l], wts->w_up[l], 2 * F, ee::ROWS_SWIGLU, 0};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wgu, d, dt, hd, c->st), "pack w_gate/w_up");
+    p = {wts->w_down[l], nullptr, d, ee::ROWS_IDENTITY, 0};
+    ok = ok && run(ee::launch_pack(p, lb + L.l_wd, F, dt, hd, c->st), "pack w_down");
+    ok = ok && run(ee::launch_copy(wts->attn_gain[l], lb + L.l_again, (size_t)d * 4, c->st), "copy gain") &&
+         run(ee::launch_copy(wts->ffn_gain[l], lb + L.l_fgain, (size_t)d * 4, c->st), "copy gain");
+  }
+  // rotary table (cos, sin) of every position, computed in double
+  std::vector<float> rope((size_t)cfg->max_ctx * hd);
+  for (int p = 0; p < cfg->max_ctx; ++p)
+    for (int i = 0; i < hd / 2; ++i) {
+      const double ang = (double)p * pow((double)cfg->rope_theta, -2.0 * i / hd);
+      rope[((size_t)p * (hd / 2) + i) * 2 + 0] = (float)cos(ang);
+      rope[((size_t)p * (hd / 2) + i) * 2 + 1] = (float)sin(ang);
+    }
+  ok = ok && run(hipMemcpyAsync(c->ws + L.rope, rope.data(), rope.size() * 4, hipMemcpyHostToDevice, c->st), "upload rope");
+  ok = ok && run(hipMemsetAsync(c->pool, 0, L.kv_total, c->st), "zero KV pool");
+  ok = ok && run(hipStreamSynchronize(c->st), "hipStreamSynchronize");
+  if (!ok) return cleanup(EE_EHIP);
+
+  ee::Model& m = c->m;
+  m.L = nl; m.d = d; m.H = H; m.Hkv = Hkv; m.hd = hd; m.F = F; m.V = cfg->vocab; m.dt = dt;
+  m.eps = cfg->rms_eps; m.max_ctx = cfg->max_ctx; m.max_pages = L.n_pages;
+  m.embed = c->packed + L.embed;
+  m.lm_head = reinterpret_cast<const uint4*>(c->packed + L.lm_head);
+  m.final_gain = reinterpret_cast<const float*>(c->packed + L.final_gain);
+  m.layers = c->layers.data();
+  m.kv_pool = c->pool;
+  m.rope = reinterpret_cast<const float2*>(c->ws + L.rope);
+  bind_work(c);
+  c->seqs.assign(cfg->max_seqs, Seq());
+  c->free_pages.clear();
+  for (int p = L.n_pages - 1; p >= 0; --p) c->free_pages.push_back(p);
+  *out = c;
+  return EE_OK;
+}
+
+int32_t ee_destroy(ee_ctx* c) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (c->st) (void)hipStreamSynchronize(c->st);
+  for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  if (c->h_stage) (void)hipHostFree(c->h_stage);
+  if (c->h_result) (void)hipHostFree(c->h_result);
+  delete c;
+  return EE_OK;
+}
+
+int32_t ee_prefill(ee_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, int32_t* next_token) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!tokens || !next_token) return fail(c, EE_EINVAL, "tokens and next_token must be non-NULL");
+  if (n < 1) return fail(c, EE_EINVAL, "prefill needs at least one token");
+  Seq& s = c->seqs[seq];
+  if (s.live) return fail(c, EE_ESTATE, "sequence already holds tokens (roll it back to 0 first)");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "token outside [0, vocab)");
+  if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "prompt longer than max_ctx - 1");
+  int added;
+  if (!reserve_pages(c, s, n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  const Layout& L = c->lay;
+  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
+  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
+  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
+  const int len0 = s.len;
+  int last = -1;
+  for (int off = 0; off < n; off += L.Tmax) {
+    const int T = std::min(L.Tmax, n - off);
+    for (int r = 0; r < T; ++r) {
+      tok[r] = tokens[off + r];
+      pos[r] = s.len + r;
+      prow[r] = r - 1;
+    }
+    rc = run_block(c, s, T, 0);
+    if (rc) {   // leave the sequence empty, as before the call
+      s.len = len0;
+      unreserve(c, s, added);
+      return rc;
+    }
+    s.len += T;
+    last = c->h_result[1];
+  }
+  s.live = true;
+  s.pending = last;
+  *next_token = last;
+  return EE_OK;
+}
+
+int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const int32_t* parent,
+                  int32_t* accept_len, int32_t* next_token, int32_t* accepted_nodes) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!accept_len || !next_token) return fail(c, EE_EINVAL, "accept_len and next_token must be non-NULL");
+  Seq& s = c->seqs[seq];
+  if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
+  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
+  if (K > 0 && !draft) return fail(c, EE_EINVAL, "draft_tokens is NULL");
+  for (int i = 0; i < K; ++i)
+    if (draft[i] < 0 || draft[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "draft token outside [0, vocab)");
+  const Layout& L = c->lay;
+  const int T = K + 1;
+  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
+  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
+  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
+  unsigned long long* anc = reinterpret_cast<unsigned long long*>(c->h_stage + L.s_anc);
+  int depth[65];
+  if (parent) {
+    depth[0] = 0;
+    for (int i = 0; i < K; ++i) {
+      if (parent[i] < -1 || parent[i] >= i) return fail(c, EE_EINVAL, "parent[i] must be in [-1, i)");
+      depth[i + 1] = depth[parent[i] + 1] + 1;
+    }
+  }
+  if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
+  int added;
+  if (!reserve_pages(c, s, s.len + T, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  tok[0] = s.pending;
+  pos[0] = s.len;
+  prow[0] = -1;
+  anc[0] = 0;
+  for (int r = 1; r < T; ++r) {
+    tok[r] = draft[r - 1];
+    if (parent) {
+      const int pr = parent[r - 1] + 1;
+      prow[r] = pr;
+      pos[r] = s.len + depth[r];
+      anc[r] = (pr >= 1 ? anc[pr] : 0ull) | (1ull << (r - 1));
+    } else {
+      prow[r] = r - 1;
+      pos[r] = s.len + r;
+      anc[r] = (r >= 2 ? anc[r - 1] : 0ull) | (1ull << (r - 1));
+    }
+  }
+  rc = run_block(c, s, T, parent ? 2 : 1);
+  if (rc) {
+    unreserve(c, s, added);
+    return rc;
+  }
+  const int a = c->h_result[0];
+  s.len += 1 + a;
+  s.pending = c->h_result[1];
+  *accept_len = a;
+  *next_token = s.pending;
+  if (accepted_nodes)
+    for (int i = 0; i < a; ++i) accepted_nodes[i] = c->h_result[2 + i] - 1;
+  return EE_OK;
+}
+
+int32_t ee_kv_rollback(ee_ctx* c, int32_t seq, int32_t new_len, int32_t pending_token) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  Seq& s = c->seqs[seq];
+  if (new_len < 0) return fail(c, EE_EINVAL, "new_len must be >= 0");
+  if (new_len > s.len) return fail(c, EE_ESTATE, "rollback beyond the committed length");
+  if (new_len == 0 && pending_token == -1) {
+    unreserve(c, s, (int)s.pages.size());
+    s = Seq();
+    return EE_OK;
+  }
+  if (pending_token < 0 || pending_token >= c->cfg.vocab)
+    return fail(c, EE_EINVAL, "pending_token outside [0, vocab)");
+  if (!s.live) return fail(c, EE_ESTATE, "sequence is empty");
+  const int keep = (new_len + PAGE - 1) / PAGE;
+  unreserve(c, s, (int)s.pages.size() - keep);
+  s.len = new_len;
+  s.pending = pending_token;
+  return EE_OK;
+}
+
+int32_t ee_seq_state(ee_ctx* c, int32_t seq, int32_t* len, int32_t* pending_token) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!len || !pending_token) return fail(c, EE_EINVAL, "outputs must be non-NULL");
+  *len = c->seqs[seq].len;
+  *pending_token = c->seqs[seq].live ? c->seqs[seq].pending : -1;
+  return EE_OK;
+}
+
+int32_t ee_get_logits(ee_ctx* c, float* host_out, int32_t rows) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (!host_out) return fail(c, EE_EINVAL, "host_out is NULL");
+  if (c->last_T == 0) return fail(c, EE_ESTATE, "no block has run yet");
+  if (rows != c->last_T) return fail(c, EE_EINVAL, "rows must equal the last block's row count");
+  HIP_TRY(c, hipMemcpyAsync(host_out, c->w.logits, (size_t)rows * c->cfg.vocab * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(c, hipStreamSynchronize(c->st));
+  return EE_OK;
+}
+
+int32_t ee_read_kv(ee_ctx* c, int32_t seq, int32_t layer, void* host_k, void* host_v) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (layer < 0 || layer >= c->cfg.n_layers) return fail(c, EE_EINVAL, "layer out of range");
+  const Seq& s = c->seqs[seq];
+  const size_t esz = c->cfg.dtype == EE_BF16 ? 2 : 4;
+  const int Hkv = c->cfg.n_kv_heads, hd = c->cfg.head_dim;
+  const size_t blk = (size_t)PAGE * hd * esz;            // one (page, kv, head) block
+  std::vector<unsigned char> page(2 * Hkv * blk);
+  for (size_t pi = 0; pi * PAGE < (size_t)s.len; ++pi) {
+    const unsigned char* src = c->pool + layer * c->lay.kv_layer + (size_t)s.pages[pi] * 2 * Hkv * blk;
+    HIP_TRY(c, hipMemcpyAsync(page.data(), src, page.size(), hipMemcpyDeviceToHost, c->st));
+    HIP_TRY(c, hipStreamSynchronize(c->st));
+    for (int sp = 0; sp < PAGE && (int)(pi * PAGE) + sp < s.len; ++sp) {
+      const size_t slot = pi * PAGE + sp;
+      for (int g = 0; g < Hkv; ++g)
+        for (int dim = 0; dim < hd; ++dim) {
+          const size_t dst = ((slot * Hkv + g) * hd + dim) * esz;
+          if (host_k)
+            memcpy(reinterpret_cast<unsigned char*>(host_k) + dst,
+                   page.data() + (0 * Hkv + g) * blk + ((size_t)sp * hd + dim) * esz, esz);
+          if (host_v)
+            memcpy(reinterpret_cast<unsigned char*>(host_v) + dst,
+                   page.data() + (1 * Hkv + g) * blk + ((size_t)dim * PAGE + sp) * esz, esz);
+        }
+    }
+  }
+  return EE_OK;
+}
+
+int32_t ee_profile(ee_ctx* c, uint32_t class_mask) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (class_mask >> ee::PC_N) return fail(c, EE_EINVAL, "unknown profiling class");
+  if (class_mask && c->events.empty()) {
+    // enough pairs for every launch of one block: 7 per layer plus a few
+    const int pairs = 8 * c->cfg.n_layers + 16;
+    c->events.resize(2 * pairs);
+    for (auto& e : c->events) {
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return hip_fail(c, r, "hipEventCreate");
+    }
+    c->ev_cls.assign(pairs, 0);
+    c->prof.ev = c->events.data();
+    c->prof.cls = c->ev_cls.data();
+    c->prof.cap = pairs;
+  }
+  c->prof.mask = class_mask;
+  return EE_OK;
+}
+
+int32_t ee_profile_read(ee_ctx* c, double* ms, int64_t* launches, int32_t reset) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  for (int i = 0; i < ee::PC_N; ++i) {
+    if (ms) ms[i] = c->prof_ms[i];
+    if (launches) launches[i] = c->prof_n[i];
+    if (reset) {
+      c->prof_ms[i] = 0.0;
+      c->prof_n[i] = 0;
+    }
+  }
+  return EE_OK;
+}
+
+const char* ee_last_error(const ee_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,112 @@
+// Internal launch interface between the host engine (engine.cpp) and the
+// gfx950 kernels (kernels.hip).  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ee {
+
+enum Dt { DT_F32 = 0, DT_BF16 = 1 };
+
+// Fragment geometry shared by the weight packer, the GEMM and the producers
+// of GEMM inputs.  One "fragment" is 16 bytes per lane of a 64-lane wave and
+// covers 16 rows x KS columns of a matrix: lane (grp = lane / 16, col =
+// lane % 16) holds row `col`, columns [s*KS + grp*KS/4, s*KS + grp*KS/4 +
+// KS/4) of super-step s.  KS = 32 for bf16 (one 16x16x32 MFMA), 16 for fp32
+// (four 16x16x4 MFMAs).
+inline int ks_of(int dt) { return dt == DT_BF16 ? 32 : 16; }
+inline int esz_of(int dt) { return dt == DT_BF16 ? 2 : 4; }
+
+// Row orders applied when packing a linear layer (dst tile row -> source row).
+enum RowMap {
+  ROWS_IDENTITY = 0,
+  ROWS_ROPE = 1,     // per head of hd rows: a 16-row tile holds 8 rotary pairs
+  ROWS_SWIGLU = 2,   // gate/up interleave: a 16-row tile holds 8 gate + 8 up rows
+};
+
+struct PackSrc {
+  const void* src0;  // logical row-major [rows, K] (ROWS_SWIGLU: the gate matrix [F, K])
+  const void* src1;  // ROWS_SWIGLU: the up matrix [F, K]; otherwise unused
+  int rows;          // destination rows written by this call (2F for ROWS_SWIGLU)
+  int map;           // RowMap
+  int dst_row0;      // first destination row (multiple of 16)
+};
+
+// Pack a logical matrix into the fragment layout
+// dst[((tile * S + s) * 64 + lane) * 16 bytes], S = K / KS.
+hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, int head_dim, hipStream_t st);
+
+// Copy/convert small arrays used as-is (embedding rows, gains).
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
+
+struct LayerPtrs {
+  const uint4* wqkv;   // packed [(H + 2 Hkv) * hd, d], q/k rows in ROWS_ROPE order
+  const uint4* wo;     // packed [d, H * hd]
+  const uint4* wgu;    // packed [2F, d] in ROWS_SWIGLU order
+  const uint4* wd;     // packed [d, F]
+  const float* attn_gain;
+  const float* ffn_gain;
+};
+
+struct Model {
+  int L, d, H, Hkv, hd, F, V, dt;
+  float eps;
+  int max_ctx, max_pages;   // pages per layer in the pool
+  const void* embed;        // [V, d] row-major, model dtype
+  const uint4* lm_head;     // packed [V, d]
+  const float* final_gain;
+  LayerPtrs* layers;        // host array of L
+  void* kv_pool;            // [L][pages][2][Hkv][64 * hd]
+  const float2* rope;       // [max_ctx][hd / 2] (cos, sin)
+};
+
+// Per-step device buffers (all inside the caller's workspace).
+struct Work {
+  float* h;                 // [Tmax, d] residual stream
+  uint4* xbuf;              // packed activations, max(d, H*hd) columns
+  uint4* zbuf;              // packed activations, F columns
+  void* q;                  // [Tmax, H, hd] model dtype
+  float* attn_part;         // [splits][Hkv][Tmax*G][hd + 2]
+  float* logits;            // [Tmax, V]
+  unsigned long long* amax; // [Tmax, V/16]
+  int* greedy;              // [Tmax]
+  int* result;              // [2 + 64]: accept_len, next, accepted rows
+  // staged per call (host -> device)
+  int* tok;                 // [Tmax]
+  int* pos;                 // [Tmax] rotary position of each row
+  int* prow;                // [Tmax] parent row (tree) or r-1
+  unsigned long long* anc;  // [Tmax] bit c-1: block row c >= 1 is an ancestor-or-self
+                            // (row 0, the pending token, is seen by every row)
+  int* ptable;              // [max_pages] page of each 64-position block
+  int max_splits;
+};
+
+// Optional per-launch timing: events recorded around launches of the classes
+// selected in `mask` (bit = EE_PROF_* class).
+struct Prof {
+  uint32_t mask = 0;
+  hipEvent_t* ev = nullptr;   // pairs: ev[2i] before, ev[2i+1] after launch i
+  int* cls = nullptr;         // class of launch i
+  int cap = 0;                // pairs available
+  int used = 0;               // pairs recorded in the current block
+  bool on(int c) const { return (mask >> c) & 1u; }
+};
+
+struct Step {
+  int T;        // rows in the block
+  int n;        // committed positions before the block
+  int mode;     // 0 prefill, 1 linear verify, 2 tree verify
+};
+
+enum ProfClass {
+  PC_NORM = 0, PC_QKV, PC_ATTN, PC_COMBINE, PC_OPROJ, PC_GATEUP, PC_DOWN, PC_LMHEAD, PC_ARGMAX,
+  PC_ACCEPT, PC_COMPACT, PC_N
+};
+
+hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
+hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
+hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
+
+}  // namespace ee
