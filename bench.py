@@ -6,7 +6,8 @@ Workload (synthetic stand-in for the paper's code-editing benchmarks): a
 prompt, and an "original code" c made from the model's own 512-token greedy
 continuation G with 5% of its positions replaced in 3-8-token spans.  Every
 timed step is one Reuse-phase step: the matcher picks where the generated
-output continues in c, K = 32 tokens of c from there are verified in one
+output continues in c (a suffix match of at least 3 tokens, else the
+position right after the last verified draft), K = 32 tokens of c from there are verified in one
 forward, and the accepted prefix plus the target's next token are emitted.
 When G has been re-created in full the sequence is rolled back to the prompt.
 The emitted stream is checked to equal G (greedy verification is lossless).
@@ -31,6 +32,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# The Reuse driver resumes at a match of at least this many generated tokens;
+# shorter (single-token) matches are frequent by chance and can move the
+# cursor past the true position in the original code.
+MIN_NGRAM = 3
 METRIC = "verified tokens/sec + verify-step latency at K=32, 7B bf16; % peak HBM BW"
 
 
@@ -154,7 +159,7 @@ def main():
 
     def reuse_step():
         gen, cur = state["gen"], state["cursor"]
-        ds, _ = ee.match_reuse(gen, code, cur)
+        ds, _ = ee.match_reuse(gen, code, cur, MIN_NGRAM, 8)
         start = ds if ds >= 0 else cur
         d = code[start:start + K]
         a, nxt, _ = eng.verify(0, d)

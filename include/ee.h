@@ -50,9 +50,9 @@ typedef struct ee_ctx ee_ctx;
 /* Shape of a Llama-style decoder (RMSNorm, rotary positions with rotate-half
  * pairs, grouped-query attention with contiguous head groups, SwiGLU FFN, no
  * biases, untied LM head).  Requirements checked by ee_create:
- *   head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ *   head_dim in {64, 128} (64 for EE_F32); n_heads % n_kv_heads == 0;
  *   d_model, ffn, n_heads*head_dim and vocab multiples of 32 (bf16) or 16 (f32);
- *   page_size == 64; 0 <= k_max <= 64; max_ctx >= 1; max_seqs >= 1.       */
+ *   page_size == 64; 0 <= k_max <= 64; 1 <= max_ctx <= 8192; max_seqs >= 1. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn, vocab;
   int32_t dtype;        /* EE_F32 or EE_BF16: weights, KV cache, GEMM inputs */
@@ -159,18 +159,20 @@ int32_t ee_read_kv(ee_ctx* ctx, int32_t seq, int32_t layer, void* host_k, void* 
 
 /* Kernel classes of one forward, for ee_profile. */
 enum {
-  EE_PROF_NORM = 0,     /* embedding gather + RMSNorm launches          */
-  EE_PROF_QKV = 1,      /* QKV GEMM + rotary + KV append                */
+  EE_PROF_NORM = 0,     /* embedding / residual add + RMSNorm launches  */
+  EE_PROF_QKV = 1,      /* QKV GEMM                                     */
   EE_PROF_ATTN = 2,     /* split attention over the paged KV cache      */
   EE_PROF_COMBINE = 3,  /* merge of the attention splits                */
-  EE_PROF_OPROJ = 4,    /* O-projection GEMM + residual                 */
-  EE_PROF_GATEUP = 5,   /* gate/up GEMM + SwiGLU                        */
-  EE_PROF_DOWN = 6,     /* down-projection GEMM + residual              */
-  EE_PROF_LMHEAD = 7,   /* LM-head GEMM + per-tile argmax partials      */
+  EE_PROF_OPROJ = 4,    /* O-projection GEMM                            */
+  EE_PROF_GATEUP = 5,   /* gate/up GEMM                                 */
+  EE_PROF_DOWN = 6,     /* down-projection GEMM                         */
+  EE_PROF_LMHEAD = 7,   /* LM-head GEMM                                 */
   EE_PROF_ARGMAX = 8,   /* vocabulary argmax                            */
   EE_PROF_ACCEPT = 9,   /* acceptance scan / tree walk                  */
   EE_PROF_COMPACT = 10, /* tree KV compaction                           */
-  EE_PROF_N = 11
+  EE_PROF_FINISH = 11,  /* GEMM epilogues: rotary + KV append, SwiGLU,  */
+                        /* logits + per-chunk maxima                    */
+  EE_PROF_N = 12
 };
 
 /* Measurement aid: when bit c of class_mask is set, every launch of kernel

@@ -70,7 +70,7 @@ ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_do
                                                  ctypes.POINTER(ctypes.c_int64), _i32])
 
 PROF_CLASSES = ("norm", "qkv", "attn", "combine", "oproj", "gateup", "down", "lmhead", "argmax",
-                "accept", "compact")
+                "accept", "compact", "finish")
 
 
 class EEError(RuntimeError):

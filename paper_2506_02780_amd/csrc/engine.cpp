@@ -39,7 +39,7 @@ struct Layout {
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
-  size_t h, xbuf, zbuf, q, part, logits, amax, greedy, result, stage, rope, ws_total;
+  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
   size_t s_tok, s_pos, s_prow, s_anc, s_ptable, stage_bytes;
   size_t kv_layer, kv_total;
@@ -53,6 +53,7 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
       c->vocab < 1)
     return bad("every model dimension must be positive");
   if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c->dtype == EE_F32 && c->head_dim != 64) return bad("fp32 models need head_dim 64");
   if (c->n_heads % c->n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
   const int ks = c->dtype == EE_BF16 ? 32 : 16;
   if (c->d_model % ks || c->ffn % ks || (c->n_heads * c->head_dim) % ks || c->vocab % ks)
@@ -60,6 +61,7 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   if (c->page_size != PAGE) return bad("page_size must be 64");
   if (c->k_max < 0 || c->k_max > 64) return bad("k_max must be in [0, 64]");
   if (c->max_ctx < 1 || c->max_seqs < 1) return bad("max_ctx and max_seqs must be positive");
+  if (c->max_ctx > 8192) return bad("max_ctx must be at most 8192");
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0");
   if ((c->n_heads / c->n_kv_heads) * (c->k_max + 1) > 64 * 16 * 16)
     return bad("too many query columns per KV head");
@@ -103,8 +105,20 @@ Layout make_layout(const ee_model_config* c) {
   L.zbuf = o; o += up(Tpad * F * esz);
   L.q = o; o += up(L.Tmax * H * hd * esz);
   L.part = o; o += up((size_t)L.max_splits * Hkv * L.Tmax * L.G * (hd + 2) * 4);
+  {
+    // split-K partials of the largest GEMM: [slices][Tmax][N]
+    const int dt = c->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
+    const size_t qkvN = (H + 2 * Hkv) * hd;
+    size_t mx = 0;
+    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * qkvN);
+    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)(H * hd), dt) * d);
+    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * 2 * F);
+    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)F, dt) * d);
+    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * V);
+    L.gpart = o; o += up(mx * L.Tmax * 4);
+  }
   L.logits = o; o += up(L.Tmax * V * 4);
-  L.amax = o; o += up(L.Tmax * (V / 16) * 8);
+  L.amax = o; o += up(L.Tmax * ((V + 2047) / 2048) * 8);
   L.greedy = o; o += up(L.Tmax * 4);
   L.result = o; o += up((2 + 64) * 4);
   // staging block: one host->device copy per call
@@ -177,6 +191,7 @@ void bind_work(ee_ctx* c) {
   w.zbuf = reinterpret_cast<uint4*>(ws + L.zbuf);
   w.q = ws + L.q;
   w.attn_part = reinterpret_cast<float*>(ws + L.part);
+  w.part = reinterpret_cast<float*>(ws + L.gpart);
   w.logits = reinterpret_cast<float*>(ws + L.logits);
   w.amax = reinterpret_cast<unsigned long long*>(ws + L.amax);
   w.greedy = reinterpret_cast<int*>(ws + L.greedy);
@@ -315,9 +330,8 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   };
   bool ok = run(ee::launch_copy(wts->embed, c->packed + L.embed, (size_t)cfg->vocab * d * esz, c->st), "copy embed") &&
             run(ee::launch_copy(wts->final_gain, c->packed + L.final_gain, (size_t)d * 4, c->st), "copy gain");
-  ee::PackSrc ps{};
-  ps.src0 = wts->lm_head; ps.rows = cfg->vocab; ps.map = ee::ROWS_IDENTITY; ps.dst_row0 = 0;
-  ok = ok && run(ee::launch_pack(ps, c->packed + L.lm_head, d, dt, hd, c->st), "pack lm_head");
+  ee::PackSrc ps{wts->lm_head, cfg->vocab, 0};
+  ok = ok && run(ee::launch_pack(ps, c->packed + L.lm_head, d, dt, c->st), "pack lm_head");
   c->layers.resize(nl);
   for (int l = 0; l < nl && ok; ++l) {
     unsigned char* lb = c->packed + L.layers0 + (size_t)l * L.per_layer;
@@ -328,19 +342,13 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
     lp.wd = reinterpret_cast<const uint4*>(lb + L.l_wd);
     lp.attn_gain = reinterpret_cast<const float*>(lb + L.l_again);
     lp.ffn_gain = reinterpret_cast<const float*>(lb + L.l_fgain);
-    ee::PackSrc p{};
-    p = {wts->wq[l], nullptr, H * hd, ee::ROWS_ROPE, 0};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wq");
-    p = {wts->wk[l], nullptr, Hkv * hd, ee::ROWS_ROPE, H * hd};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wk");
-    p = {wts->wv[l], nullptr, Hkv * hd, ee::ROWS_IDENTITY, (H + Hkv) * hd};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, hd, c->st), "pack wv");
-    p = {wts->wo[l], nullptr, d, ee::ROWS_IDENTITY, 0};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wo, H * hd, dt, hd, c->st), "pack wo");
-    p = {wts->w_gate[l], wts->w_up[l], 2 * F, ee::ROWS_SWIGLU, 0};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wgu, d, dt, hd, c->st), "pack w_gate/w_up");
-    p = {wts->w_down[l], nullptr, d, ee::ROWS_IDENTITY, 0};
-    ok = ok && run(ee::launch_pack(p, lb + L.l_wd, F, dt, hd, c->st), "pack w_down");
+    const ee::PackSrc parts[] = {
+        {wts->wq[l], H * hd, 0}, {wts->wk[l], Hkv * hd, H * hd}, {wts->wv[l], Hkv * hd, (H + Hkv) * hd}};
+    for (const auto& p : parts) ok = ok && run(ee::launch_pack(p, lb + L.l_wqkv, d, dt, c->st), "pack wqkv");
+    ok = ok && run(ee::launch_pack({wts->wo[l], d, 0}, lb + L.l_wo, H * hd, dt, c->st), "pack wo");
+    ok = ok && run(ee::launch_pack({wts->w_gate[l], F, 0}, lb + L.l_wgu, d, dt, c->st), "pack w_gate");
+    ok = ok && run(ee::launch_pack({wts->w_up[l], F, F}, lb + L.l_wgu, d, dt, c->st), "pack w_up");
+    ok = ok && run(ee::launch_pack({wts->w_down[l], d, 0}, lb + L.l_wd, F, dt, c->st), "pack w_down");
     ok = ok && run(ee::launch_copy(wts->attn_gain[l], lb + L.l_again, (size_t)d * 4, c->st), "copy gain") &&
          run(ee::launch_copy(wts->ffn_gain[l], lb + L.l_fgain, (size_t)d * 4, c->st), "copy gain");
   }

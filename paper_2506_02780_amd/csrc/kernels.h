@@ -19,32 +19,26 @@ enum Dt { DT_F32 = 0, DT_BF16 = 1 };
 inline int ks_of(int dt) { return dt == DT_BF16 ? 32 : 16; }
 inline int esz_of(int dt) { return dt == DT_BF16 ? 2 : 4; }
 
-// Row orders applied when packing a linear layer (dst tile row -> source row).
-enum RowMap {
-  ROWS_IDENTITY = 0,
-  ROWS_ROPE = 1,     // per head of hd rows: a 16-row tile holds 8 rotary pairs
-  ROWS_SWIGLU = 2,   // gate/up interleave: a 16-row tile holds 8 gate + 8 up rows
-};
-
 struct PackSrc {
-  const void* src0;  // logical row-major [rows, K] (ROWS_SWIGLU: the gate matrix [F, K])
-  const void* src1;  // ROWS_SWIGLU: the up matrix [F, K]; otherwise unused
-  int rows;          // destination rows written by this call (2F for ROWS_SWIGLU)
-  int map;           // RowMap
+  const void* src;   // logical row-major [rows, K]
+  int rows;          // rows copied (multiple of 16)
   int dst_row0;      // first destination row (multiple of 16)
 };
 
 // Pack a logical matrix into the fragment layout
 // dst[((tile * S + s) * 64 + lane) * 16 bytes], S = K / KS.
-hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, int head_dim, hipStream_t st);
+hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, hipStream_t st);
+
+// K-slices of the split-K GEMM for a reduction length K (depends on K only).
+int gemm_slices_for(int K, int dt);
 
 // Copy/convert small arrays used as-is (embedding rows, gains).
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
 struct LayerPtrs {
-  const uint4* wqkv;   // packed [(H + 2 Hkv) * hd, d], q/k rows in ROWS_ROPE order
+  const uint4* wqkv;   // packed [(H + 2 Hkv) * hd, d]: q rows, k rows, v rows
   const uint4* wo;     // packed [d, H * hd]
-  const uint4* wgu;    // packed [2F, d] in ROWS_SWIGLU order
+  const uint4* wgu;    // packed [2F, d]: gate rows, then up rows
   const uint4* wd;     // packed [d, F]
   const float* attn_gain;
   const float* ffn_gain;
@@ -69,8 +63,9 @@ struct Work {
   uint4* zbuf;              // packed activations, F columns
   void* q;                  // [Tmax, H, hd] model dtype
   float* attn_part;         // [splits][Hkv][Tmax*G][hd + 2]
+  float* part;              // GEMM slice partials [SK][T][N]
   float* logits;            // [Tmax, V]
-  unsigned long long* amax; // [Tmax, V/16]
+  unsigned long long* amax; // [Tmax, ceil(V/2048)]
   int* greedy;              // [Tmax]
   int* result;              // [2 + 64]: accept_len, next, accepted rows
   // staged per call (host -> device)
@@ -102,7 +97,7 @@ struct Step {
 
 enum ProfClass {
   PC_NORM = 0, PC_QKV, PC_ATTN, PC_COMBINE, PC_OPROJ, PC_GATEUP, PC_DOWN, PC_LMHEAD, PC_ARGMAX,
-  PC_ACCEPT, PC_COMPACT, PC_N
+  PC_ACCEPT, PC_COMPACT, PC_FINISH, PC_N
 };
 
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);

@@ -31,11 +31,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Streaming 16-byte load (weights are read once per step).
-__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
 
 // ---------------------------------------------------------------- numerics --
 
@@ -97,32 +92,13 @@ template <int DT> __device__ __forceinline__ size_t frag_index(int row, int col,
 
 // ------------------------------------------------------------------ packing --
 
-// Destination row r of a packed layer -> source row, per RowMap.
-__device__ __forceinline__ int map_row(int map, int r, int hd, int* sel) {
-  *sel = 0;
-  if (map == ROWS_IDENTITY) return r;
-  const int tile = r >> 4, rr = r & 15, grp = rr >> 2, q = rr & 3;
-  if (map == ROWS_ROPE) {
-    // rows of head h: tile j of the head holds pairs i = 8j + 2grp + (q & 1),
-    // rows q = 0,1 the first half, q = 2,3 the partner i + hd/2.
-    const int tiles_per_head = hd >> 4;
-    const int head = tile / tiles_per_head, j = tile % tiles_per_head;
-    const int i = 8 * j + 2 * grp + (q & 1);
-    return head * hd + i + ((q >> 1) ? (hd >> 1) : 0);
-  }
-  // ROWS_SWIGLU: tile j holds features f = 8j + 2grp + (q & 1); q = 0,1 gate, 2,3 up
-  *sel = q >> 1;
-  return 8 * tile + 2 * grp + (q & 1);
-}
-
 template <int DT>
-__global__ void pack_kernel(const void* __restrict__ src0, const void* __restrict__ src1,
-                            int map, int rows_in_call, int dst_row0, int K, int hd,
+__global__ void pack_kernel(const void* __restrict__ src, int rows, int dst_row0, int K,
                             uint4* __restrict__ dst) {
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL;
   const int S = K / KS;
   // one thread per destination lane-fragment (16 bytes)
-  const size_t frags = (size_t)rows_in_call / 16 * S * 64;
+  const size_t frags = (size_t)rows / 16 * S * 64;
   for (size_t f = blockIdx.x * (size_t)blockDim.x + threadIdx.x; f < frags;
        f += (size_t)gridDim.x * blockDim.x) {
     const int lane = (int)(f & 63);
@@ -130,10 +106,7 @@ __global__ void pack_kernel(const void* __restrict__ src0, const void* __restric
     const int s = (int)(ts % S);
     const int tile_local = (int)(ts / S);
     const int grp = lane >> 4, c = lane & 15;
-    const int r_local = tile_local * 16 + c;     // row within this call's block
-    int sel;
-    const int sr = map_row(map, r_local, hd, &sel);
-    const void* src = sel ? src1 : src0;
+    const int sr = tile_local * 16 + c;
     const int col0 = s * KS + grp * EPL;   // EPL elements = 16 bytes, 16-byte aligned
     const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const unsigned char*>(src) +
                                                     ((size_t)sr * K + col0) * Geo<DT>::ESZ);
@@ -142,7 +115,7 @@ __global__ void pack_kernel(const void* __restrict__ src0, const void* __restric
   }
 }
 
-hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, int head_dim, hipStream_t st) {
+hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, hipStream_t st) {
   const int ks = ks_of(dt);
   if (K % ks || ps.rows % 16 || ps.dst_row0 % 16) return hipErrorInvalidValue;
   const size_t frags = (size_t)ps.rows / 16 * (K / ks) * 64;
@@ -150,11 +123,11 @@ hipError_t launch_pack(const PackSrc& ps, void* dst, int K, int dt, int head_dim
   const size_t want = (frags + threads - 1) / threads;
   const int blocks = (int)(want < 65536 ? want : 65536);
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(pack_kernel<DT_BF16>, dim3(blocks), dim3(threads), 0, st, ps.src0, ps.src1,
-                       ps.map, ps.rows, ps.dst_row0, K, head_dim, reinterpret_cast<uint4*>(dst));
+    hipLaunchKernelGGL(pack_kernel<DT_BF16>, dim3(blocks), dim3(threads), 0, st, ps.src, ps.rows,
+                       ps.dst_row0, K, reinterpret_cast<uint4*>(dst));
   else
-    hipLaunchKernelGGL(pack_kernel<DT_F32>, dim3(blocks), dim3(threads), 0, st, ps.src0, ps.src1,
-                       ps.map, ps.rows, ps.dst_row0, K, head_dim, reinterpret_cast<uint4*>(dst));
+    hipLaunchKernelGGL(pack_kernel<DT_F32>, dim3(blocks), dim3(threads), 0, st, ps.src, ps.rows,
+                       ps.dst_row0, K, reinterpret_cast<uint4*>(dst));
   return hipGetLastError();
 }
 
@@ -163,189 +136,154 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t st)
 }
 
 // -------------------------------------------------------------------- GEMM --
+//
+// Y[t, n] = sum_k X[t, k] W[n, k] for T <= 80 rows, split over K:
+//   * the reduction dimension (S super-steps of KS columns) is cut into SK
+//     slices of SS super-steps; SK depends only on (N, K);
+//   * a workgroup (8 waves) owns one slice and a set of 16-feature tiles;
+//     wave w accumulates the slice's super-steps w, w+8, w+16, ... in order,
+//     holding its activation fragments in registers for the whole kernel and
+//     streaming weight fragments one tile ahead;
+//   * the 8 wave partials of a tile are summed in wave order and stored as
+//     part[k][t][n]; the consumer kernel adds the SK slices in slice order.
+// The arithmetic of an output element therefore never depends on T or on
+// which workgroup computed it.
 
-enum Epi { EPI_LOGITS = 0, EPI_RESIDUAL = 1, EPI_QKV = 2, EPI_SWIGLU = 3 };
+constexpr int GEMM_WAVES = 8;
+constexpr int GEMM_SPW = 8;           // super-steps per wave per slice (max)
+constexpr unsigned OOB = 0x80000000u; // buffer offset past every range: loads 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer load; offsets beyond the resource size return zeros without
+// a memory access.  AUX selects the cache policy (2 = non-temporal).
+template <int AUX>
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 struct GemmArgs {
-  const uint4* w;       // packed weights, S super-steps per tile
-  const uint4* x;       // packed activations (same S)
-  int S;
-  int T;
-  int n_tiles;
-  // epilogue outputs
-  float* out;           // EPI_LOGITS: logits [T][N]; EPI_RESIDUAL: h [T][N]
-  int N;
-  unsigned long long* amax;  // EPI_LOGITS: [T][n_tiles]
-  void* z;              // EPI_SWIGLU: packed activations of the down projection
-  int z_S;
-  // EPI_QKV
-  void* q;              // [T][H][hd]
-  void* kv_layer;       // pool base of this layer: [pages][2][Hkv][64*hd]
-  const int* ptable;
-  const int* pos;
-  const float2* rope;
-  int n;                // committed positions (block row r lands in slot n + r)
-  int H, Hkv, hd;
+  const uint4* w;       // packed weights [n_tiles][S][64]
+  const uint4* x;       // packed activations [MT][S][64]
+  float* part;          // [SK][T][N]
+  int S, SK, SS, T, N, n_tiles;
 };
 
-// One workgroup = one 16-feature tile over the whole reduction dimension.
-template <int DT, int MT, int KW, int EPI>
-__global__ __launch_bounds__(KW * 64) void gemm_kernel(GemmArgs a) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int tile = blockIdx.x;
-  const int c = lane & 15;
-  const int S = a.S;
-  const uint4* __restrict__ wp = a.w + (size_t)tile * S * 64 + lane;
-  const uint4* __restrict__ xp = a.x + lane;
+inline int gemm_slices(int S) {
+  int sk = 1;
+  while (S > GEMM_SPW * GEMM_WAVES * sk) sk *= 2;
+  return sk;
+}
 
-  bool rowok[MT];
+template <int DT, int MT>
+__global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, c = lane & 15;
+  const int k = blockIdx.x % a.SK, groups = gridDim.x / a.SK;
+  const int S = a.S, s0 = k * a.SS, ns = min(S - s0, a.SS);
+  const auto xs = make_rsrc(a.x, (unsigned)(MT * S * 1024));
+  const auto ws = make_rsrc(a.w, (unsigned)((size_t)a.n_tiles * S * 1024));
+  uint4 xr[GEMM_SPW][MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) rowok[m] = (m * 16 + c) < a.T;
-
-  f32x4 acc[MT];
+  for (int i = 0; i < GEMM_SPW; ++i) {
+    const int sl = wv + GEMM_WAVES * i;
 #pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  constexpr int U = 4;
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  int s = wv;
-  for (; s + (U - 1) * KW < S; s += U * KW) {
-    uint4 wf[U];
-    uint4 xf[U][MT];
-#pragma unroll
-    for (int u = 0; u < U; ++u) wf[u] = ld_stream(wp + (size_t)(s + u * KW) * 64);
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-        xf[u][m] = rowok[m] ? xp[((size_t)m * S + s + u * KW) * 64] : zero;
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int m = 0; m < MT; ++m) acc[m] = mma<DT>(wf[u], xf[u][m], acc[m]);
+    for (int m = 0; m < MT; ++m)
+      xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < a.T)
+                                  ? (unsigned)(((m * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
-  for (; s < S; s += KW) {
-    const uint4 wf = ld_stream(wp + (size_t)s * 64);
+  __shared__ f32x4 red[2][GEMM_WAVES][MT][64];
+  uint4 wr[GEMM_SPW];
+  int tile = blockIdx.x / a.SK;
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const uint4 xf = rowok[m] ? xp[((size_t)m * S + s) * 64] : zero;
-      acc[m] = mma<DT>(wf, xf, acc[m]);
-    }
+  for (int i = 0; i < GEMM_SPW; ++i) {
+    const int sl = wv + GEMM_WAVES * i;
+    wr[i] = bload<2>(ws, (tile < a.n_tiles && sl < ns)
+                             ? (unsigned)(((tile * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
-
-  // Sum the KW partial tiles in wave order.
-  __shared__ f32x4 red[KW][MT][64];
-  __shared__ float tileY[MT * 16][17];   // [row t][feature within tile]
+  for (int it = 0; tile < a.n_tiles; tile += groups, ++it) {
+    const int tn = tile + groups;
+    f32x4 acc[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) red[wv][m][lane] = acc[m];
-  __syncthreads();
-  for (int i = threadIdx.x; i < MT * 64; i += KW * 64) {
-    const int m = i >> 6, ln = i & 63;
-    f32x4 v = red[0][m][ln];
-    for (int k = 1; k < KW; ++k) v += red[k][m][ln];
-    const int t = m * 16 + (ln & 15), f0 = 4 * (ln >> 4);
-    tileY[t][f0 + 0] = v[0];
-    tileY[t][f0 + 1] = v[1];
-    tileY[t][f0 + 2] = v[2];
-    tileY[t][f0 + 3] = v[3];
-  }
-  __syncthreads();
-
-  const int T = a.T;
-  if (EPI == EPI_LOGITS) {
-    for (int i = threadIdx.x; i < T * 16; i += KW * 64) {
-      const int t = i >> 4, f = i & 15;
-      a.out[(size_t)t * a.N + tile * 16 + f] = tileY[t][f];
+    for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < GEMM_SPW; ++i) {
+      const uint4 wf = wr[i];
+      const int sl = wv + GEMM_WAVES * i;
+      wr[i] = bload<2>(ws, (tn < a.n_tiles && sl < ns)
+                               ? (unsigned)(((tn * S + s0 + sl) * 64 + lane) * 16) : OOB);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m] = mma<DT>(wf, xr[i][m], acc[m]);
     }
-    for (int t = threadIdx.x; t < T; t += KW * 64) {
-      unsigned long long best = 0;
-      for (int f = 0; f < 16; ++f) {
-        float v = tileY[t][f];
-        uint32_t u = __float_as_uint(v);
-        if ((u & 0x7fffffffu) > 0x7f800000u) continue;   // NaN never wins
-        if ((u & 0x7fffffffu) == 0) u = 0;                // -0 ties with +0
-        const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-        const unsigned long long key =
-            ((unsigned long long)ord << 32) | (0xffffffffu - (uint32_t)(tile * 16 + f));
-        best = key > best ? key : best;
-      }
-      a.amax[(size_t)t * a.n_tiles + tile] = best;
-    }
-  } else if (EPI == EPI_RESIDUAL) {
-    for (int i = threadIdx.x; i < T * 16; i += KW * 64) {
-      const int t = i >> 4, f = i & 15;
-      a.out[(size_t)t * a.N + tile * 16 + f] += tileY[t][f];
-    }
-  } else if (EPI == EPI_SWIGLU) {
-    // tile j, lane group grp, q: feature 8j + 2grp + (q & 1); q = 0,1 gate, q = 2,3 up
-    for (int i = threadIdx.x; i < T * 8; i += KW * 64) {
-      const int t = i >> 3, p = i & 7, grp = p >> 1, e = p & 1;
-      const float gte = tileY[t][4 * grp + e], up = tileY[t][4 * grp + 2 + e];
-      const float zv = gte / (1.0f + expf(-gte)) * up;
-      const int f = 8 * tile + 2 * grp + e;
-      store_elt<DT>(a.z, frag_index<DT>(t, f, a.z_S), zv);
-    }
-  } else {  // EPI_QKV
-    const int hd = a.hd, half = hd >> 1;
-    const int row0 = tile * 16;                       // packed row of this tile
-    const int qrows = a.H * hd, krows = a.Hkv * hd;
-    for (int i = threadIdx.x; i < T * 8; i += KW * 64) {
-      const int t = i >> 3, p = i & 7, grp = p >> 1, e = p & 1;
-      const int slot = a.n + t;
-      const int page = a.ptable[slot >> 6], sp = slot & 63;
-      if (row0 < qrows + krows) {
-        // rotary pair: rows 4grp + e (first half) and 4grp + 2 + e (partner)
-        const bool isq = row0 < qrows;
-        const int base = isq ? row0 : row0 - qrows;
-        const int head = base / hd, j = (base % hd) >> 4;
-        const int di = 8 * j + 2 * grp + e;
-        const float2 cs = a.rope[(size_t)a.pos[t] * half + di];
-        const float x1 = tileY[t][4 * grp + e], x2 = tileY[t][4 * grp + 2 + e];
-        const float y1 = x1 * cs.x - x2 * cs.y;
-        const float y2 = x2 * cs.x + x1 * cs.y;
-        if (isq) {
-          const size_t qb = ((size_t)t * a.H + head) * hd;
-          store_elt<DT>(a.q, qb + di, y1);
-          store_elt<DT>(a.q, qb + di + half, y2);
-        } else {
-          const size_t kb = (((size_t)page * 2 + 0) * a.Hkv + head) * 64 * hd + (size_t)sp * hd;
-          store_elt<DT>(a.kv_layer, kb + di, y1);
-          store_elt<DT>(a.kv_layer, kb + di + half, y2);
-        }
-      } else {
-        const int base = row0 - qrows - krows;
-        const int head = base / hd, d0 = base % hd;
-        // value rows are in natural order: tile row rr is dim d0 + rr; V stored [dim][slot]
-        const size_t vb = (((size_t)page * 2 + 1) * a.Hkv + head) * 64 * hd;
-        const int r1 = 4 * grp + e, r2 = 4 * grp + 2 + e;
-        store_elt<DT>(a.kv_layer, vb + (size_t)(d0 + r1) * 64 + sp, tileY[t][r1]);
-        store_elt<DT>(a.kv_layer, vb + (size_t)(d0 + r2) * 64 + sp, tileY[t][r2]);
+    const int pb = it & 1;   // two reduction buffers: one barrier per tile
+#pragma unroll
+    for (int m = 0; m < MT; ++m) red[pb][wv][m][lane] = acc[m];
+    __syncthreads();
+    for (int q = threadIdx.x; q < MT * 64; q += GEMM_WAVES * 64) {
+      const int m = q >> 6, ln = q & 63;
+      f32x4 v = red[pb][0][m][ln];
+#pragma unroll
+      for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][m][ln];
+      const int t = m * 16 + (ln & 15);
+      if (t < a.T) {
+        float* o = a.part + ((size_t)k * a.T + t) * a.N + tile * 16 + 4 * (ln >> 4);
+        *reinterpret_cast<float4*>(o) = make_float4(v.x, v.y, v.z, v.w);
       }
     }
   }
 }
 
-template <int DT, int EPI, int KW>
-static hipError_t gemm_dispatch_mt(const GemmArgs& a, hipStream_t st) {
-  const int mt = (a.T + 15) / 16;
-  const dim3 grid(a.n_tiles), block(KW * 64);
-  switch (mt) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1, KW, EPI>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2, KW, EPI>), grid, block, 0, st, a); break;
-    case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3, KW, EPI>), grid, block, 0, st, a); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4, KW, EPI>), grid, block, 0, st, a); break;
-    case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5, KW, EPI>), grid, block, 0, st, a); break;
+template <int DT>
+static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int T, float* part,
+                       hipStream_t st) {
+  GemmArgs a;
+  a.w = w; a.x = x; a.part = part; a.T = T; a.N = N;
+  a.S = K / Geo<DT>::KS;
+  a.SK = gemm_slices(a.S);
+  a.SS = (a.S + a.SK - 1) / a.SK;
+  a.n_tiles = N / 16;
+  int groups = 256 / a.SK;
+  if (groups < 1) groups = 1;
+  if (groups > a.n_tiles) groups = a.n_tiles;
+  const dim3 grid(groups * a.SK), block(GEMM_WAVES * 64);
+  switch ((T + 15) / 16) {
+    case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4>), grid, block, 0, st, a); break;
+    case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5>), grid, block, 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int DT, int EPI>
-static hipError_t gemm(const GemmArgs& a, hipStream_t st) {
-  // waves per tile depend only on the reduction length, never on T
-  if (a.S >= 256) return gemm_dispatch_mt<DT, EPI, 8>(a, st);
-  if (a.S >= 64) return gemm_dispatch_mt<DT, EPI, 4>(a, st);
-  return gemm_dispatch_mt<DT, EPI, 2>(a, st);
+// Sum of the SK slice partials of element (t, n), in slice order.
+__device__ __forceinline__ float4 sum_slices4(const float* __restrict__ part, int SK, int T, int N,
+                                              int t, int n) {
+  float4 v = *reinterpret_cast<const float4*>(part + (size_t)t * N + n);
+  for (int k = 1; k < SK; ++k) {
+    const float4 u = *reinterpret_cast<const float4*>(part + ((size_t)k * T + t) * N + n);
+    v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+  }
+  return v;
+}
+
+// Pack 8 consecutive values of row t starting at column col (col % 8 == 0)
+// into the fragment layout: one 16-byte store for bf16, two for fp32.
+template <int DT>
+__device__ __forceinline__ void store8(void* xout, int t, int col, int S, const float* v) {
+  if (DT == DT_BF16) {
+    const uint4 u = make_uint4(f2bf_bits(v[0]) | (f2bf_bits(v[1]) << 16),
+                               f2bf_bits(v[2]) | (f2bf_bits(v[3]) << 16),
+                               f2bf_bits(v[4]) | (f2bf_bits(v[5]) << 16),
+                               f2bf_bits(v[6]) | (f2bf_bits(v[7]) << 16));
+    *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(xout) + frag_index<DT>(t, col, S)) = u;
+  } else {
+    float* f = reinterpret_cast<float*>(xout);
+    *reinterpret_cast<float4*>(f + frag_index<DT>(t, col, S)) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(f + frag_index<DT>(t, col + 4, S)) = make_float4(v[4], v[5], v[6], v[7]);
+  }
 }
 
 // ------------------------------------------------------------ embed / norm --
@@ -363,28 +301,157 @@ __device__ __forceinline__ float block_sum256(float v, float* sh) {
   return r;
 }
 
-// Row t: optionally h = E[tok[t]]; x = RMSNorm(h) * gain -> packed activation.
-template <int DT, bool EMBED>
+// Row t of the residual stream: h = E[tok[t]] (MODE 0) or h += sum of the
+// GEMM slice partials (MODE 1); then x = RMSNorm(h) * gain, packed as the
+// next GEMM's activations.  Each thread owns 8-column chunks (d % 8 == 0).
+template <int DT, int MODE>
 __global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ embed,
                                                    const int* __restrict__ tok, float* __restrict__ h,
+                                                   const float* __restrict__ part, int SK, int T,
                                                    const float* __restrict__ gain, float eps, int d,
                                                    void* __restrict__ xout, int x_S) {
   __shared__ float sh[256];
   const int t = blockIdx.x;
   float* hr = h + (size_t)t * d;
-  if (EMBED) {
-    const size_t e0 = (size_t)tok[t] * d;
-    for (int i = threadIdx.x; i < d; i += 256) hr[i] = load_elt<DT>(embed, e0 + i);
-  }
+  const int nch = d / 8;
+  constexpr int MAXCH = 4;               // d <= 8192
+  float v[MAXCH][8];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    const float v = hr[i];
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int j = 0; j < MAXCH; ++j) {
+    const int ch = threadIdx.x + 256 * j;
+    if (ch >= nch) break;
+    const int col = ch * 8;
+    if (MODE == 0) {
+      const size_t e0 = (size_t)tok[t] * d + col;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[j][e] = load_elt<DT>(embed, e0 + e);
+    } else {
+      const float4 h0 = *reinterpret_cast<const float4*>(hr + col);
+      const float4 h1 = *reinterpret_cast<const float4*>(hr + col + 4);
+      const float4 p0 = sum_slices4(part, SK, T, d, t, col);
+      const float4 p1 = sum_slices4(part, SK, T, d, t, col + 4);
+      v[j][0] = h0.x + p0.x; v[j][1] = h0.y + p0.y; v[j][2] = h0.z + p0.z; v[j][3] = h0.w + p0.w;
+      v[j][4] = h1.x + p1.x; v[j][5] = h1.y + p1.y; v[j][6] = h1.z + p1.z; v[j][7] = h1.w + p1.w;
+    }
+    *reinterpret_cast<float4*>(hr + col) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+    *reinterpret_cast<float4*>(hr + col + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(v[j][e], v[j][e], ss);
   }
   ss = block_sum256(ss, sh);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256)
-    store_elt<DT>(xout, frag_index<DT>(t, i, x_S), hr[i] * r * gain[i]);
+#pragma unroll
+  for (int j = 0; j < MAXCH; ++j) {
+    const int ch = threadIdx.x + 256 * j;
+    if (ch >= nch) break;
+    const int col = ch * 8;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = v[j][e] * r * gain[col + e];
+    store8<DT>(xout, t, col, x_S, o);
+  }
+}
+
+// q/k/v of row t from the QKV partials: rotary on q and k (pairs (i, i+hd/2)
+// at the row's position), q to the block buffer, k and v into the row's KV
+// cache slot n + t (V stored transposed per page).  One thread per pair.
+template <int DT>
+__global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict__ part, int SK, int T,
+                                                         int N, int H, int Hkv, int hd,
+                                                         const int* __restrict__ pos,
+                                                         const float2* __restrict__ rope,
+                                                         const int* __restrict__ ptable, int n,
+                                                         void* __restrict__ q, void* __restrict__ kv_layer) {
+  const int t = blockIdx.y;
+  const int half = hd >> 1;
+  const int pairs = (H + 2 * Hkv) * half;
+  const int p = blockIdx.x * 256 + threadIdx.x;
+  if (p >= pairs) return;
+  const int head = p / half, i = p % half;       // head over [q heads | k heads | v heads]
+  const int f1 = head * hd + i, f2 = f1 + half;
+  float x1 = part[(size_t)t * N + f1], x2 = part[(size_t)t * N + f2];
+  for (int k = 1; k < SK; ++k) {
+    x1 += part[((size_t)k * T + t) * N + f1];
+    x2 += part[((size_t)k * T + t) * N + f2];
+  }
+  const int slot = n + t;
+  const int page = ptable[slot >> 6], sp = slot & 63;
+  if (head < H + Hkv) {
+    const float2 cs = rope[(size_t)pos[t] * half + i];
+    const float y1 = x1 * cs.x - x2 * cs.y;
+    const float y2 = x2 * cs.x + x1 * cs.y;
+    if (head < H) {
+      const size_t qb = ((size_t)t * H + head) * hd;
+      store_elt<DT>(q, qb + i, y1);
+      store_elt<DT>(q, qb + i + half, y2);
+    } else {
+      const size_t kb = (((size_t)page * 2 + 0) * Hkv + (head - H)) * 64 * hd + (size_t)sp * hd;
+      store_elt<DT>(kv_layer, kb + i, y1);
+      store_elt<DT>(kv_layer, kb + i + half, y2);
+    }
+  } else {
+    const size_t vb = (((size_t)page * 2 + 1) * Hkv + (head - H - Hkv)) * 64 * hd;
+    store_elt<DT>(kv_layer, vb + (size_t)i * 64 + sp, x1);
+    store_elt<DT>(kv_layer, vb + (size_t)(i + half) * 64 + sp, x2);
+  }
+}
+
+// z = silu(gate) * up from the gate/up partials (rows [0, F) gate, [F, 2F)
+// up), packed as the down projection's activations.  8 features per thread.
+template <int DT>
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ part, int SK, int T, int F,
+                                                     void* __restrict__ zout, int z_S) {
+  const int t = blockIdx.y;
+  const int ch = blockIdx.x * 256 + threadIdx.x;
+  if (ch * 8 >= F) return;
+  const int f = ch * 8, N = 2 * F;
+  const float4 g0 = sum_slices4(part, SK, T, N, t, f), g1 = sum_slices4(part, SK, T, N, t, f + 4);
+  const float4 u0 = sum_slices4(part, SK, T, N, t, F + f), u1 = sum_slices4(part, SK, T, N, t, F + f + 4);
+  const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+  const float u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+  float z[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) z[e] = g[e] / (1.0f + expf(-g[e])) * u[e];
+  store8<DT>(zout, t, f, z_S, z);
+}
+
+// Logits of row t from the LM-head partials, plus the (value, -index) maximum
+// of each 2048-column chunk.
+__device__ __forceinline__ unsigned long long amax_key(float v, int idx) {
+  uint32_t u = __float_as_uint(v);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0ull;   // NaN never wins
+  if ((u & 0x7fffffffu) == 0) u = 0;                   // -0 ties with +0
+  const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)ord << 32) | (0xffffffffu - (uint32_t)idx);
+}
+
+__global__ __launch_bounds__(256) void logits_kernel(const float* __restrict__ part, int SK, int T, int V,
+                                                     float* __restrict__ logits,
+                                                     unsigned long long* __restrict__ amax, int nchunk) {
+  __shared__ unsigned long long sh[256];
+  const int t = blockIdx.y;
+  const int col = (blockIdx.x * 256 + threadIdx.x) * 8;
+  unsigned long long best = 0;
+  if (col < V) {
+    const float4 a = sum_slices4(part, SK, T, V, t, col), b = sum_slices4(part, SK, T, V, t, col + 4);
+    float* lr = logits + (size_t)t * V + col;
+    *reinterpret_cast<float4*>(lr) = a;
+    *reinterpret_cast<float4*>(lr + 4) = b;
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const unsigned long long kk = amax_key(v[e], col + e);
+      best = kk > best ? kk : best;
+    }
+  }
+  sh[threadIdx.x] = best;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w && sh[threadIdx.x + w] > sh[threadIdx.x]) sh[threadIdx.x] = sh[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) amax[(size_t)t * nchunk + blockIdx.x] = sh[0];
 }
 
 // --------------------------------------------------------------- attention --
@@ -399,32 +466,113 @@ struct AttnArgs {
   int tree;
   float scale_log2;         // log2(e) / sqrt(hd)
   float* part;              // [splits][Hkv][ncols][hd + 2]
+  int max_pages;            // pages per layer in the pool
+  int wpg;                  // q-tiles per workgroup
 };
 
-constexpr int SPLIT = 256;  // keys per split (4 sub-tiles of 64)
+constexpr int SPLIT = 256;   // keys per split (4 sub-tiles of 64)
+constexpr int NSUB = SPLIT / 64;
+constexpr int ATT_THREADS = 1024;
+
+// LDS layout of one split: K rows [NSUB][64][HD] and V^T [NSUB][HD][64], rows
+// padded by 16 bytes to spread banks.
+template <int DT, int HD> struct AttnLds {
+  static constexpr int ESZ = Geo<DT>::ESZ;
+  static constexpr int ROWB = HD * ESZ, KROW = ROWB + 16, VROW = 64 * ESZ + 16;
+  static constexpr int KSUB = 64 * KROW, VSUB = HD * VROW;
+  static constexpr int BYTES = NSUB * (KSUB + VSUB);
+  static constexpr int UNITS = 2 * 64 * HD * ESZ / 16;             // uint4 per sub-tile (K + V)
+  static constexpr int PER = (NSUB * UNITS + ATT_THREADS - 1) / ATT_THREADS;
+};
 
 template <int DT, int HD>
-__global__ __launch_bounds__(1024) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
+  using LY = AttnLds<DT, HD>;
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
   constexpr int NS = HD / KS;          // fragments along head_dim
   constexpr int ND = HD / 16;          // output dim tiles
-  constexpr int ROWB = HD * ESZ;       // bytes of one key row
-  constexpr int KROW = ROWB + 16;      // padded LDS row strides (bank spread)
-  constexpr int VROW = 64 * ESZ + 16;
-  __shared__ __attribute__((aligned(16))) unsigned char Ks[64 * KROW];
-  __shared__ __attribute__((aligned(16))) unsigned char Vt[HD * VROW];
+  constexpr int ROWB = LY::ROWB, KROW = LY::KROW, VROW = LY::VROW;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LY::BYTES];
+  unsigned char* Kall = lds;
+  unsigned char* Vall = lds + NSUB * LY::KSUB;
 
   const int sp = blockIdx.x, gkv = blockIdx.y, qgrp = blockIdx.z;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, c = lane & 15;
-  const int qt = qgrp * nw + wv;
+  const int nkeys = a.n + a.T;          // slots written so far
+  const int base0 = sp * SPLIT;
+  const int nsub = min(NSUB, (nkeys - base0 + 63) / 64);
+
+  // ---- stage every sub-tile of the split with one batch of loads ----
+  {
+    const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
+    const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
+    constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
+    uint4 tmp[LY::PER];
+    unsigned dst[LY::PER];
+#pragma unroll
+    for (int j = 0; j < LY::PER; ++j) {
+      const int idx = threadIdx.x + j * ATT_THREADS;
+      const int st = idx / LY::UNITS, rem = idx % LY::UNITS;
+      const int kv = rem / HALF, u = rem % HALF;
+      unsigned off = OOB;
+      dst[j] = 0xffffffffu;
+      if (st < nsub) {
+        const int base = base0 + st * 64;
+        const int page = a.ptable[base >> 6];
+        const int valid = nkeys - base;
+        off = (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ + (size_t)u * 16);
+        if (kv == 0) {
+          const int row = u / (ROWB / 16), col = u % (ROWB / 16);
+          if (row >= valid) off = OOB;                    // unwritten slots read as zeros
+          dst[j] = st * LY::KSUB + row * KROW + col * 16;
+        } else {
+          constexpr int VU = 64 * ESZ / 16;               // uint4 per V^T row
+          dst[j] = NSUB * LY::KSUB + st * LY::VSUB + (u / VU) * VROW + (u % VU) * 16;
+          dst[j] |= (unsigned)min(valid, 64) << 24;       // remember the valid key count
+        }
+      }
+      tmp[j] = bload<0>(rs, off);
+    }
+#pragma unroll
+    for (int j = 0; j < LY::PER; ++j) {
+      if (dst[j] == 0xffffffffu) continue;
+      unsigned d = dst[j];
+      uint4 v = tmp[j];
+      if (d >= (unsigned)(NSUB * LY::KSUB) && (d >> 24) != 0) {
+        // V^T chunk: zero the key columns beyond the written slots
+        const int valid = (int)(d >> 24);
+        d &= 0x00ffffffu;
+        if (valid < 64) {
+          const int col0 = (((d - NSUB * LY::KSUB) % LY::VSUB) % VROW) / ESZ;
+          if (DT == DT_BF16) {
+            uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+            for (int e = 0; e < 8; ++e)
+              if (col0 + e >= valid) w4[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+            v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+          } else {
+            if (col0 + 0 >= valid) v.x = 0;
+            if (col0 + 1 >= valid) v.y = 0;
+            if (col0 + 2 >= valid) v.z = 0;
+            if (col0 + 3 >= valid) v.w = 0;
+          }
+        }
+      }
+      *reinterpret_cast<uint4*>(lds + d) = v;
+    }
+  }
+  __syncthreads();
+
+  const int nqt = (a.ncols + 15) / 16;
+  const int qt = qgrp * a.wpg + wv;
+  if (wv >= a.wpg || qt >= nqt) return;   // no barrier follows
+
   const int qc = qt * 16 + c;
   const bool colok = qc < a.ncols;
   const int t = colok ? qc / a.G : 0;
   const int head = gkv * a.G + (colok ? qc % a.G : 0);
   const int mypos = colok ? a.pos[t] : -1;
   const unsigned long long myanc = (colok && a.tree) ? a.anc[t] : 0ull;
-  const int nkeys = a.n + a.T;          // slots written so far
 
   // query fragments (B operand): column qc, head dims [s*KS + grp*EPL, +EPL)
   uint4 qf[NS];
@@ -442,45 +590,10 @@ __global__ __launch_bounds__(1024) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < ND; ++i) o_run[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const size_t head_stride = (size_t)64 * HD;   // elements per (page, kv, head) block
-  for (int st = 0; st < SPLIT / 64; ++st) {
-    const int base = sp * SPLIT + st * 64;
-    if (base >= nkeys) break;
-    const int page = a.ptable[base >> 6];
-    const unsigned char* kg = reinterpret_cast<const unsigned char*>(a.kv_layer) +
-                              ((((size_t)page * 2 + 0) * a.Hkv + gkv) * head_stride) * ESZ;
-    const unsigned char* vg = reinterpret_cast<const unsigned char*>(a.kv_layer) +
-                              ((((size_t)page * 2 + 1) * a.Hkv + gkv) * head_stride) * ESZ;
-    const int valid = nkeys - base;    // keys in this sub-tile that were written
-    // K rows [64][HD]: zero rows >= valid
-    for (int i = threadIdx.x; i < 64 * ROWB / 16; i += blockDim.x) {
-      const int row = i / (ROWB / 16), col = i % (ROWB / 16);
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row < valid) v = *reinterpret_cast<const uint4*>(kg + (size_t)i * 16);
-      *reinterpret_cast<uint4*>(Ks + row * KROW + col * 16) = v;
-    }
-    // V^T [HD][64]: zero columns >= valid
-    for (int i = threadIdx.x; i < HD * 64 * ESZ / 16; i += blockDim.x) {
-      uint4 v = *reinterpret_cast<const uint4*>(vg + (size_t)i * 16);
-      if (valid < 64) {
-        const int col0 = ((i * 16) / ESZ) & 63;   // 16 bytes never straddle a dim row
-        if (DT == DT_BF16) {
-          uint32_t w[4] = {v.x, v.y, v.z, v.w};
-          for (int e = 0; e < 8; ++e)
-            if (col0 + e >= valid) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-          v = make_uint4(w[0], w[1], w[2], w[3]);
-        } else {
-          if (col0 + 0 >= valid) v.x = 0;
-          if (col0 + 1 >= valid) v.y = 0;
-          if (col0 + 2 >= valid) v.z = 0;
-          if (col0 + 3 >= valid) v.w = 0;
-        }
-      }
-      constexpr int VU = 64 * ESZ / 16;   // uint4 per V^T row
-      *reinterpret_cast<uint4*>(Vt + (i / VU) * VROW + (i % VU) * 16) = v;
-    }
-    __syncthreads();
-
+  for (int st = 0; st < nsub; ++st) {
+    const int base = base0 + st * 64;
+    const unsigned char* Ks = Kall + st * LY::KSUB;
+    const unsigned char* Vt = Vall + st * LY::VSUB;
     // S^T = K Q^T for 4 key tiles of 16: lane holds key 16kt + 4grp + r, column c
     f32x4 sacc[4];
 #pragma unroll
@@ -573,7 +686,6 @@ __global__ __launch_bounds__(1024) void attn_kernel(AttnArgs a) {
         }
       }
     }
-    __syncthreads();
   }
 
   if (colok) {
@@ -589,30 +701,51 @@ __global__ __launch_bounds__(1024) void attn_kernel(AttnArgs a) {
   }
 }
 
+constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
+
 // Merge the splits of every (row, head) in split order; write the attention
-// output as packed activations of the O projection.
+// output as packed activations of the O projection.  4 dims per thread.
 template <int DT, int HD>
-__global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
-                                                         int Hkv, int G, int ncols, int H,
-                                                         void* __restrict__ xout, int x_S) {
+__global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
+                                                              int Hkv, int G, int ncols, int H,
+                                                              void* __restrict__ xout, int x_S) {
   const int t = blockIdx.x / H, j = blockIdx.x % H;
   const int gkv = j / G, qc = t * G + (j % G);
-  const int dim = threadIdx.x;
+  const int dim = threadIdx.x * 4;
+  float ms[MAX_SPLITS], ls[MAX_SPLITS];
   float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) {
-    const float* p = part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2);
-    if (p[HD + 1] > 0.f) M = fmaxf(M, p[HD]);
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s) {
+    ms[s] = -INFINITY;
+    ls[s] = 0.f;
+    if (s < nsplit) {
+      const float* p = part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2);
+      ms[s] = p[HD];
+      ls[s] = p[HD + 1];
+      if (ls[s] > 0.f) M = fmaxf(M, ms[s]);
+    }
   }
-  float L = 0.f, O = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float* p = part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2);
-    const float l = p[HD + 1];
-    if (!(l > 0.f)) continue;
-    const float w = exp2f(p[HD] - M);
-    L = fmaf(l, w, L);
-    O = fmaf(p[dim], w, O);
+  float L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s) {
+    if (s >= nsplit || !(ls[s] > 0.f)) continue;
+    const float w = exp2f(ms[s] - M);
+    const float4 o = *reinterpret_cast<const float4*>(part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2) + dim);
+    L = fmaf(ls[s], w, L);
+    O[0] = fmaf(o.x, w, O[0]);
+    O[1] = fmaf(o.y, w, O[1]);
+    O[2] = fmaf(o.z, w, O[2]);
+    O[3] = fmaf(o.w, w, O[3]);
   }
-  store_elt<DT>(xout, frag_index<DT>(t, j * HD + dim, x_S), O / L);
+  const size_t fi = frag_index<DT>(t, j * HD + dim, x_S);
+  if (DT == DT_BF16) {
+    const uint2 u = make_uint2(f2bf_bits(O[0] / L) | (f2bf_bits(O[1] / L) << 16),
+                               f2bf_bits(O[2] / L) | (f2bf_bits(O[3] / L) << 16));
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(xout) + fi) = u;
+  } else {
+    *reinterpret_cast<float4*>(reinterpret_cast<float*>(xout) + fi) =
+        make_float4(O[0] / L, O[1] / L, O[2] / L, O[3] / L);
+  }
 }
 
 // ------------------------------------------------------- argmax and accept --
@@ -737,18 +870,21 @@ static hipError_t timed(Prof* prof, int c, hipStream_t st, F&& launch) {
   return hipSuccess;
 }
 
+int gemm_slices_for(int K, int dt) { return gemm_slices(K / ks_of(dt)); }
+
 template <int DT, int HD>
 static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   constexpr int KS = Geo<DT>::KS;
-  const int T = s.T, d = m.d, qdim = m.H * m.hd;
+  const int T = s.T, d = m.d, qdim = m.H * m.hd, qkvN = qdim + 2 * m.Hkv * m.hd;
   const int Sd = d / KS, Sq = qdim / KS, Sf = m.F / KS;
+  const int sk_d = gemm_slices(Sd), sk_q = gemm_slices(Sq), sk_f = gemm_slices(Sf);
   const size_t layer_elems = (size_t)m.max_pages * 2 * m.Hkv * 64 * m.hd;
   hipError_t e;
   auto last = [] { return hipGetLastError(); };
 
   if ((e = timed(prof, PC_NORM, st, [&] {
-         hipLaunchKernelGGL((norm_kernel<DT, true>), dim3(T), dim3(256), 0, st, m.embed, w.tok, w.h,
-                            m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
+         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(T), dim3(256), 0, st, m.embed, w.tok, w.h,
+                            w.part, 1, T, m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
          return last();
        })) != hipSuccess)
     return e;
@@ -758,18 +894,21 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   const int nsplit = (nkeys + SPLIT - 1) / SPLIT;
   const int nqt = (ncols + 15) / 16;
   const int nqg = (nqt + 15) / 16;
-  const int wpb = (nqt + nqg - 1) / nqg;
+  const int wpb = (nqt + nqg - 1) / nqg;   // q-tiles per workgroup (<= 16 waves)
+  const int pairs = (m.H + 2 * m.Hkv) * (m.hd / 2);
 
   for (int l = 0; l < m.L; ++l) {
     const LayerPtrs& lp = m.layers[l];
     void* kvl = reinterpret_cast<unsigned char*>(m.kv_pool) + l * layer_elems * Geo<DT>::ESZ;
-    GemmArgs g{};
-    g.T = T;
-    // QKV + rotary + KV append
-    g.w = lp.wqkv; g.x = w.xbuf; g.S = Sd; g.n_tiles = (qdim + 2 * m.Hkv * m.hd) / 16;
-    g.q = w.q; g.kv_layer = kvl; g.ptable = w.ptable; g.pos = w.pos; g.rope = m.rope; g.n = s.n;
-    g.H = m.H; g.Hkv = m.Hkv; g.hd = m.hd;
-    if ((e = timed(prof, PC_QKV, st, [&] { return gemm<DT, EPI_QKV>(g, st); })) != hipSuccess) return e;
+    // QKV projection, then rotary + KV append
+    if ((e = timed(prof, PC_QKV, st, [&] { return gemm<DT>(lp.wqkv, w.xbuf, qkvN, d, T, w.part, st); })) != hipSuccess)
+      return e;
+    if ((e = timed(prof, PC_FINISH, st, [&] {
+           hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, T), dim3(256), 0, st, w.part,
+                              sk_d, T, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.ptable, s.n, w.q, kvl);
+           return last();
+         })) != hipSuccess)
+      return e;
     // attention
     AttnArgs aa{};
     aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.anc = w.anc;
@@ -777,52 +916,60 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     aa.tree = s.mode == 2;
     aa.scale_log2 = 1.4426950408889634f / sqrtf((float)m.hd);
     aa.part = w.attn_part;
+    aa.max_pages = m.max_pages;
+    aa.wpg = wpb;
     if ((e = timed(prof, PC_ATTN, st, [&] {
-           hipLaunchKernelGGL((attn_kernel<DT, HD>), dim3(nsplit, m.Hkv, nqg), dim3(wpb * 64), 0, st, aa);
+           hipLaunchKernelGGL((attn_kernel<DT, HD>), dim3(nsplit, m.Hkv, nqg), dim3(ATT_THREADS), 0, st, aa);
            return last();
          })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
-           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(T * m.H), dim3(HD), 0, st, w.attn_part,
+           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(T * m.H), dim3(HD / 4), 0, st, w.attn_part,
                               nsplit, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
       return e;
-    // O projection + residual
-    g = GemmArgs{};
-    g.T = T; g.w = lp.wo; g.x = w.xbuf; g.S = Sq; g.n_tiles = d / 16; g.out = w.h; g.N = d;
-    if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT, EPI_RESIDUAL>(g, st); })) != hipSuccess) return e;
-    // FFN norm
+    // O projection; residual add + FFN norm
+    if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, T, w.part, st); })) != hipSuccess)
+      return e;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, false>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h,
-                              lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h, w.part,
+                              sk_q, T, lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
       return e;
-    // gate/up + SwiGLU
-    g = GemmArgs{};
-    g.T = T; g.w = lp.wgu; g.x = w.xbuf; g.S = Sd; g.n_tiles = 2 * m.F / 16; g.z = w.zbuf; g.z_S = Sf;
-    if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT, EPI_SWIGLU>(g, st); })) != hipSuccess) return e;
-    // down + residual
-    g = GemmArgs{};
-    g.T = T; g.w = lp.wd; g.x = w.zbuf; g.S = Sf; g.n_tiles = d / 16; g.out = w.h; g.N = d;
-    if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT, EPI_RESIDUAL>(g, st); })) != hipSuccess) return e;
-    // next norm: attention side of layer l+1, or the final norm
+    // gate/up projection, then SwiGLU
+    if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT>(lp.wgu, w.xbuf, 2 * m.F, d, T, w.part, st); })) != hipSuccess)
+      return e;
+    if ((e = timed(prof, PC_FINISH, st, [&] {
+           hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, T), dim3(256), 0, st, w.part, sk_d,
+                              T, m.F, (void*)w.zbuf, Sf);
+           return last();
+         })) != hipSuccess)
+      return e;
+    // down projection; residual add + the next norm (layer l+1 attention side, or final)
+    if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT>(lp.wd, w.zbuf, d, m.F, T, w.part, st); })) != hipSuccess)
+      return e;
     const float* gn = (l + 1 < m.L) ? m.layers[l + 1].attn_gain : m.final_gain;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, false>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h,
-                              gn, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h, w.part,
+                              sk_f, T, gn, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
       return e;
   }
-  // LM head + argmax partials
-  GemmArgs g{};
-  g.T = T; g.w = m.lm_head; g.x = w.xbuf; g.S = Sd; g.n_tiles = m.V / 16; g.out = w.logits; g.N = m.V;
-  g.amax = w.amax;
-  if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT, EPI_LOGITS>(g, st); })) != hipSuccess) return e;
+  // LM head, logits + chunk maxima, argmax
+  if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, T, w.part, st); })) != hipSuccess)
+    return e;
+  const int nchunk = (m.V + 2047) / 2048;
+  if ((e = timed(prof, PC_FINISH, st, [&] {
+         hipLaunchKernelGGL(logits_kernel, dim3(nchunk, T), dim3(256), 0, st, w.part, sk_d, T, m.V, w.logits,
+                            w.amax, nchunk);
+         return last();
+       })) != hipSuccess)
+    return e;
   return timed(prof, PC_ARGMAX, st, [&] {
-    hipLaunchKernelGGL(argmax_kernel, dim3(T), dim3(256), 0, st, w.amax, m.V / 16, w.greedy);
+    hipLaunchKernelGGL(argmax_kernel, dim3(T), dim3(256), 0, st, w.amax, nchunk, w.greedy);
     return last();
   });
 }
@@ -830,7 +977,6 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   if (m.dt == DT_BF16 && m.hd == 128) return forward_t<DT_BF16, 128>(m, w, s, prof, st);
   if (m.dt == DT_BF16 && m.hd == 64) return forward_t<DT_BF16, 64>(m, w, s, prof, st);
-  if (m.dt == DT_F32 && m.hd == 128) return forward_t<DT_F32, 128>(m, w, s, prof, st);
   if (m.dt == DT_F32 && m.hd == 64) return forward_t<DT_F32, 64>(m, w, s, prof, st);
   return hipErrorInvalidValue;
 }
