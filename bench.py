@@ -57,10 +57,10 @@ def step_bytes(s, t: int, n: int) -> dict:
 
 
 def gateup_bytes(s, t: int) -> int:
-    """Algorithmic bytes of one gate/up GEMM launch: the [2F, d] weights, the
-    T normalised input rows and the T SwiGLU output rows."""
+    """Algorithmic bytes of one gate/up GEMM launch: the [2F, d] weights and
+    the T normalised input rows it multiplies."""
     esz = 2 if s.dtype == "bf16" else 4
-    return esz * (2 * s.ffn * s.d_model + t * s.d_model + t * s.ffn)
+    return esz * (2 * s.ffn * s.d_model + t * s.d_model)
 
 
 def cpu_baseline(shape, weights, k: int, ctx: int, layers: int, emitted_per_step: float):
@@ -177,8 +177,6 @@ def main():
     reset()
     for _ in range(args.warmup):
         reuse_step()
-    eng.profile(["gateup"])
-    eng.profile_read(reset=True)
     torch.cuda.synchronize()
     emitted, lat = 0, []
     t_start = time.perf_counter()
@@ -188,6 +186,14 @@ def main():
         lat.append(time.perf_counter() - ts)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+
+    # dominant kernel: the same session continues for as many steps with HIP
+    # events around every gate/up GEMM launch (events inside a replayed graph
+    # cannot be timed, so these steps launch kernel by kernel)
+    eng.profile(["gateup"])
+    eng.profile_read(reset=True)
+    for _ in range(args.steps):
+        reuse_step()
     prof = eng.profile_read(reset=True)
     eng.profile([])
     gu_ms, gu_n = prof["gateup"]
@@ -241,7 +247,8 @@ def main():
         "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4)},
         "roofline": {
-            "kernel": "gemm_kernel (gate/up projection + SwiGLU epilogue)",
+            "kernel": "gemm_kernel<bf16, MT=3> (gate/up projection, T=33)",
+            "measured": "HIP events around each gate/up launch over a second run of the timed workload",
             "bound": "hbm",
             "achieved": round(gu_alg / gu_avg_s / 1e9, 1),
             "peak": HBM_PEAK_GBS,

@@ -157,6 +157,12 @@ int32_t ee_get_logits(ee_ctx* ctx, float* host_out, int32_t rows);
  * dtype (fp32 or bf16 bits).  Either output may be NULL.  Test aid. */
 int32_t ee_read_kv(ee_ctx* ctx, int32_t seq, int32_t layer, void* host_k, void* host_v);
 
+/* Launch mode of later prefill/verify blocks.  on != 0 (the default): the
+ * kernels of each block shape (row count, linear/tree/prefill) are captured
+ * once into a HIP graph and replayed; on == 0: every kernel is launched
+ * individually.  Both run the same kernels with the same arguments. */
+int32_t ee_use_graphs(ee_ctx* ctx, int32_t on);
+
 /* Kernel classes of one forward, for ee_profile. */
 enum {
   EE_PROF_NORM = 0,     /* embedding / residual add + RMSNorm launches  */
@@ -178,8 +184,8 @@ enum {
 /* Measurement aid: when bit c of class_mask is set, every launch of kernel
  * class c is bracketed by two HIP events on the context's stream, and the
  * elapsed time between them is accumulated after each prefill / verify
- * block.  class_mask = 0 turns it off (the default).  The events add a small
- * overhead to the instrumented launches only. */
+ * block.  class_mask = 0 turns it off (the default).  While it is on, blocks
+ * are launched kernel by kernel (no graph replay). */
 int32_t ee_profile(ee_ctx* ctx, uint32_t class_mask);
 
 /* Read the accumulated per-class totals: ms[EE_PROF_N] milliseconds and

@@ -66,6 +66,7 @@ ee_get_logits = _sig("ee_get_logits", _i32, [_vp, ctypes.POINTER(ctypes.c_float)
 ee_read_kv = _sig("ee_read_kv", _i32, [_vp, _i32, _i32, _vp, _vp])
 ee_last_error = _sig("ee_last_error", ctypes.c_char_p, [_vp])
 ee_profile = _sig("ee_profile", _i32, [_vp, ctypes.c_uint32])
+ee_use_graphs = _sig("ee_use_graphs", _i32, [_vp, _i32])
 ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(ctypes.c_int64), _i32])
 
@@ -212,6 +213,10 @@ class Engine:
         v = np.empty_like(k)
         _check(ee_read_kv(self.ctx, seq, layer, k.ctypes.data, v.ctypes.data), self.ctx)
         return k, v
+
+    def use_graphs(self, on: bool):
+        """Replay captured HIP graphs per block shape (default) or launch eagerly."""
+        _check(ee_use_graphs(self.ctx, int(bool(on))), self.ctx)
 
     def profile(self, classes=()):
         """Bracket launches of the named kernel classes with HIP events."""

@@ -8,6 +8,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <map>
+#include <tuple>
 #include <new>
 #include <string>
 #include <vector>
@@ -41,7 +43,7 @@ struct Layout {
   // workspace
   size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
-  size_t s_tok, s_pos, s_prow, s_anc, s_ptable, stage_bytes;
+  size_t s_tok, s_pos, s_prow, s_anc, s_ptable, s_info, stage_bytes;
   size_t kv_layer, kv_total;
 };
 
@@ -56,6 +58,8 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   if (c->dtype == EE_F32 && c->head_dim != 64) return bad("fp32 models need head_dim 64");
   if (c->n_heads % c->n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
   const int ks = c->dtype == EE_BF16 ? 32 : 16;
+  if (c->d_model > 8192 || c->ffn > 32768 || c->n_heads * c->head_dim > 32768)
+    return bad("d_model <= 8192, ffn and n_heads*head_dim <= 32768");
   if (c->d_model % ks || c->ffn % ks || (c->n_heads * c->head_dim) % ks || c->vocab % ks)
     return bad("d_model, ffn, n_heads*head_dim and vocab must be multiples of 32 (bf16) / 16 (f32)");
   if (c->page_size != PAGE) return bad("page_size must be 64");
@@ -128,6 +132,7 @@ Layout make_layout(const ee_model_config* c) {
   L.s_pos = so; so += L.Tmax * 4;
   L.s_prow = so; so += L.Tmax * 4;
   L.s_ptable = so; so += L.pages_per_seq * 4;
+  L.s_info = so; so += 4 * 4;
   L.stage_bytes = up(so);
   L.stage = o; o += L.stage_bytes;
   L.rope = o; o += up((size_t)c->max_ctx * (hd / 2) * 8);
@@ -144,7 +149,16 @@ Layout make_layout(const ee_model_config* c) {
 struct ee_ctx {
   ee_model_config cfg;
   Layout lay;
-  hipStream_t st = nullptr;
+  hipStream_t user_st = nullptr;     // caller's stream (ee_create work)
+  hipStream_t st = nullptr;          // library stream of every later call
+  hipEvent_t ev_user = nullptr;      // orders `st` after the caller's stream
+  struct Captured {
+    hipGraphExec_t exec;
+    int prof_pairs;                  // event pairs recorded by the graph's own nodes
+  };
+  std::map<std::tuple<int, int, uint32_t>, Captured> graphs;   // (T, mode, profiling mask)
+  bool graphs_ok = true;             // capture works on this stream
+  bool graphs_on = true;             // ee_use_graphs
   unsigned char* packed = nullptr;
   unsigned char* pool = nullptr;
   unsigned char* ws = nullptr;
@@ -202,6 +216,7 @@ void bind_work(ee_ctx* c) {
   w.pos = reinterpret_cast<int*>(sb + L.s_pos);
   w.prow = reinterpret_cast<int*>(sb + L.s_prow);
   w.ptable = reinterpret_cast<int*>(sb + L.s_ptable);
+  w.info = reinterpret_cast<int*>(sb + L.s_info);
   w.max_splits = L.max_splits;
 }
 
@@ -234,19 +249,68 @@ int check_seq(ee_ctx* c, int seq) {
   return EE_OK;
 }
 
+// The kernels of one block, in launch order.
+hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
+  hipError_t e;
+  if ((e = ee::run_forward(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
+  if ((e = ee::run_accept(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
+  if (step.mode == 2 && (e = ee::run_compact(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
+  return hipSuccess;
+}
+
+// Captured graph of a (T, mode) block shape, built on first use (profiling
+// events, when enabled, become event-record nodes of the graph); nullptr if
+// capture is unavailable (the block then runs eagerly).
+const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
+  if (!c->graphs_ok || !c->graphs_on) return nullptr;
+  const auto key = std::make_tuple(step.T, step.mode, prof ? prof->mask : 0u);
+  auto it = c->graphs.find(key);
+  if (it != c->graphs.end()) return &it->second;
+  hipGraph_t g = nullptr;
+  hipGraphExec_t ge = nullptr;
+  if (hipStreamBeginCapture(c->st, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+    c->graphs_ok = false;
+    return nullptr;
+  }
+  if (prof) prof->used = 0;
+  const hipError_t le = launch_block(c, step, prof);
+  const hipError_t ce = hipStreamEndCapture(c->st, &g);
+  if (le != hipSuccess || ce != hipSuccess || !g || hipGraphInstantiate(&ge, g, nullptr, nullptr, 0) != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();
+    c->graphs_ok = false;
+    return nullptr;
+  }
+  (void)hipGraphDestroy(g);
+  auto& slot = c->graphs[key];
+  slot.exec = ge;
+  slot.prof_pairs = prof ? prof->used : 0;
+  return &slot;
+}
+
 // Stage rows, run the forward + acceptance (+ tree compaction), fetch the
 // result.  Returns EE_OK and fills h_result.
 int run_block(ee_ctx* c, Seq& s, int T, int mode) {
   const Layout& L = c->lay;
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
   for (size_t i = 0; i < s.pages.size(); ++i) ptab[i] = s.pages[i];
+  int* info = reinterpret_cast<int*>(c->h_stage + L.s_info);
+  info[0] = s.len;
+  info[1] = (s.len + T + SPLIT - 1) / SPLIT;
+  HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
+  HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
   HIP_TRY(c, hipMemcpyAsync(c->ws + L.stage, c->h_stage, L.stage_bytes, hipMemcpyHostToDevice, c->st));
-  ee::Step step{T, s.len, mode};
+  const ee::Step step{T, mode};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
-  c->prof.used = 0;
-  HIP_TRY(c, ee::run_forward(c->m, c->w, step, prof, c->st));
-  HIP_TRY(c, ee::run_accept(c->m, c->w, step, prof, c->st));
-  if (mode == 2) HIP_TRY(c, ee::run_compact(c->m, c->w, step, prof, c->st));
+  // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
+  const ee_ctx::Captured* cg = prof ? nullptr : block_graph(c, step, nullptr);
+  if (cg) {
+    HIP_TRY(c, hipGraphLaunch(cg->exec, c->st));
+    c->prof.used = cg->prof_pairs;
+  } else {
+    c->prof.used = 0;
+    HIP_TRY(c, launch_block(c, step, prof));
+  }
   HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (2 + 64) * sizeof(int), hipMemcpyDeviceToHost, c->st));
   HIP_TRY(c, hipStreamSynchronize(c->st));
   for (int i = 0; prof && i < c->prof.used; ++i) {
@@ -299,7 +363,8 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   if (!c) return fail(nullptr, EE_EINVAL, "out of host memory");
   c->cfg = *cfg;
   c->lay = make_layout(cfg);
-  c->st = reinterpret_cast<hipStream_t>(hip_stream);
+  c->user_st = reinterpret_cast<hipStream_t>(hip_stream);
+  c->st = c->user_st;   // packing runs on the caller's stream
   c->packed = reinterpret_cast<unsigned char*>(packed);
   c->pool = reinterpret_cast<unsigned char*>(kv_pool);
   c->ws = reinterpret_cast<unsigned char*>(workspace);
@@ -309,6 +374,7 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   const int d = cfg->d_model, hd = cfg->head_dim, H = cfg->n_heads, Hkv = cfg->n_kv_heads, F = cfg->ffn;
 
   auto cleanup = [&](int code) {
+    if (c->ev_user) (void)hipEventDestroy(c->ev_user);
     if (c->h_stage) (void)hipHostFree(c->h_stage);
     if (c->h_result) (void)hipHostFree(c->h_result);
     g_err = c->err;
@@ -364,6 +430,15 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   ok = ok && run(hipMemsetAsync(c->pool, 0, L.kv_total, c->st), "zero KV pool");
   ok = ok && run(hipStreamSynchronize(c->st), "hipStreamSynchronize");
   if (!ok) return cleanup(EE_EHIP);
+  // every later call runs on a library stream (capturable; the legacy default
+  // stream is not), ordered after the caller's stream at the start of a call
+  hipStream_t own = nullptr;
+  if (!run(hipStreamCreateWithFlags(&own, hipStreamNonBlocking), "hipStreamCreate") ||
+      !run(hipEventCreateWithFlags(&c->ev_user, hipEventDisableTiming), "hipEventCreate")) {
+    if (own) (void)hipStreamDestroy(own);
+    return cleanup(EE_EHIP);
+  }
+  c->st = own;
 
   ee::Model& m = c->m;
   m.L = nl; m.d = d; m.H = H; m.Hkv = Hkv; m.hd = hd; m.F = F; m.V = cfg->vocab; m.dt = dt;
@@ -385,7 +460,10 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
 int32_t ee_destroy(ee_ctx* c) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
   if (c->st) (void)hipStreamSynchronize(c->st);
+  for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second.exec);
   for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  if (c->ev_user) (void)hipEventDestroy(c->ev_user);
+  if (c->st && c->st != c->user_st) (void)hipStreamDestroy(c->st);
   if (c->h_stage) (void)hipHostFree(c->h_stage);
   if (c->h_result) (void)hipHostFree(c->h_result);
   delete c;
@@ -559,6 +637,12 @@ int32_t ee_read_kv(ee_ctx* c, int32_t seq, int32_t layer, void* host_k, void* ho
         }
     }
   }
+  return EE_OK;
+}
+
+int32_t ee_use_graphs(ee_ctx* c, int32_t on) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  c->graphs_on = on != 0;
   return EE_OK;
 }
 

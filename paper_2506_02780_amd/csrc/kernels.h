@@ -75,7 +75,8 @@ struct Work {
   unsigned long long* anc;  // [Tmax] bit c-1: block row c >= 1 is an ancestor-or-self
                             // (row 0, the pending token, is seen by every row)
   int* ptable;              // [max_pages] page of each 64-position block
-  int max_splits;
+  int* info;                // [0] committed positions n, [1] attention splits in use
+  int max_splits;           // attention splits of the longest context
 };
 
 // Optional per-launch timing: events recorded around launches of the classes
@@ -89,9 +90,12 @@ struct Prof {
   bool on(int c) const { return (mask >> c) & 1u; }
 };
 
+// Launch shape of one block.  Everything that changes from step to step
+// (committed length, split count, tokens, positions, pages) is read by the
+// kernels from the staging block, so a captured graph of a (T, mode) shape
+// can be replayed for any step.
 struct Step {
   int T;        // rows in the block
-  int n;        // committed positions before the block
   int mode;     // 0 prefill, 1 linear verify, 2 tree verify
 };
 

@@ -41,6 +41,11 @@ __device__ __forceinline__ uint32_t f2bf_bits(float f) {
   return u >> 16;
 }
 __device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+// Nearest-even bf16 bits of a finite float (no NaN handling, no branch).
+__device__ __forceinline__ uint32_t f2bf_bits_finite(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
 
 // Round a float to the storage type and return the stored value as float.
 template <int DT> __device__ __forceinline__ float rnd(float x);
@@ -174,7 +179,7 @@ struct GemmArgs {
 inline int gemm_slices(int S) {
   int sk = 1;
   while (S > GEMM_SPW * GEMM_WAVES * sk) sk *= 2;
-  return sk;
+  return sk;   // <= 16 for every K the library accepts (K <= 32768)
 }
 
 template <int DT, int MT>
@@ -258,14 +263,20 @@ static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int T, floa
   return hipGetLastError();
 }
 
-// Sum of the SK slice partials of element (t, n), in slice order.
+constexpr int MAX_SLICES = 16;   // gemm_slices() never exceeds this for K <= 32768
+
+// Sum of the SK slice partials of elements (t, n..n+3), in slice order.  All
+// loads are issued before the first add (no dependent round trips).
 __device__ __forceinline__ float4 sum_slices4(const float* __restrict__ part, int SK, int T, int N,
                                               int t, int n) {
-  float4 v = *reinterpret_cast<const float4*>(part + (size_t)t * N + n);
-  for (int k = 1; k < SK; ++k) {
-    const float4 u = *reinterpret_cast<const float4*>(part + ((size_t)k * T + t) * N + n);
-    v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
-  }
+  float4 u[MAX_SLICES];
+#pragma unroll
+  for (int k = 0; k < MAX_SLICES; ++k)
+    if (k < SK) u[k] = *reinterpret_cast<const float4*>(part + ((size_t)k * T + t) * N + n);
+  float4 v = u[0];
+#pragma unroll
+  for (int k = 1; k < MAX_SLICES; ++k)
+    if (k < SK) { v.x += u[k].x; v.y += u[k].y; v.z += u[k].z; v.w += u[k].w; }
   return v;
 }
 
@@ -361,7 +372,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
                                                          int N, int H, int Hkv, int hd,
                                                          const int* __restrict__ pos,
                                                          const float2* __restrict__ rope,
-                                                         const int* __restrict__ ptable, int n,
+                                                         const int* __restrict__ ptable,
+                                                         const int* __restrict__ info,
                                                          void* __restrict__ q, void* __restrict__ kv_layer) {
   const int t = blockIdx.y;
   const int half = hd >> 1;
@@ -370,12 +382,18 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
   if (p >= pairs) return;
   const int head = p / half, i = p % half;       // head over [q heads | k heads | v heads]
   const int f1 = head * hd + i, f2 = f1 + half;
-  float x1 = part[(size_t)t * N + f1], x2 = part[(size_t)t * N + f2];
-  for (int k = 1; k < SK; ++k) {
-    x1 += part[((size_t)k * T + t) * N + f1];
-    x2 += part[((size_t)k * T + t) * N + f2];
-  }
-  const int slot = n + t;
+  float p1[MAX_SLICES], p2[MAX_SLICES];
+#pragma unroll
+  for (int k = 0; k < MAX_SLICES; ++k)
+    if (k < SK) {
+      p1[k] = part[((size_t)k * T + t) * N + f1];
+      p2[k] = part[((size_t)k * T + t) * N + f2];
+    }
+  float x1 = p1[0], x2 = p2[0];
+#pragma unroll
+  for (int k = 1; k < MAX_SLICES; ++k)
+    if (k < SK) { x1 += p1[k]; x2 += p2[k]; }
+  const int slot = info[0] + t;   // block row t lands in slot n + t
   const int page = ptable[slot >> 6], sp = slot & 63;
   if (head < H + Hkv) {
     const float2 cs = rope[(size_t)pos[t] * half + i];
@@ -462,30 +480,49 @@ struct AttnArgs {
   const int* ptable;
   const int* pos;
   const unsigned long long* anc;
-  int T, n, H, Hkv, G, ncols;
+  const int* info;          // [0] committed positions n, [1] splits in use
+  int T, H, Hkv, G, ncols;
   int tree;
   float scale_log2;         // log2(e) / sqrt(hd)
   float* part;              // [splits][Hkv][ncols][hd + 2]
   int max_pages;            // pages per layer in the pool
-  int wpg;                  // q-tiles per workgroup
 };
 
 constexpr int SPLIT = 256;   // keys per split (4 sub-tiles of 64)
 constexpr int NSUB = SPLIT / 64;
-constexpr int ATT_THREADS = 1024;
 
-// LDS layout of one split: K rows [NSUB][64][HD] and V^T [NSUB][HD][64], rows
+template <int AUX>
+__device__ __forceinline__ uint2 bload64(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
+  return make_uint2(v.x, v.y);
+}
+
+constexpr int ATT_THREADS = 1024;
+constexpr int ATT_QT = ATT_THREADS / 64 / NSUB;   // query tiles per workgroup
+
+// LDS image of one split: K rows [NSUB][64][HD] and V^T [NSUB][HD][64], rows
 // padded by 16 bytes to spread banks.
 template <int DT, int HD> struct AttnLds {
   static constexpr int ESZ = Geo<DT>::ESZ;
   static constexpr int ROWB = HD * ESZ, KROW = ROWB + 16, VROW = 64 * ESZ + 16;
   static constexpr int KSUB = 64 * KROW, VSUB = HD * VROW;
-  static constexpr int BYTES = NSUB * (KSUB + VSUB);
+  static constexpr int KV_BYTES = NSUB * (KSUB + VSUB);
+  static constexpr int ST_BYTES = (ATT_THREADS / 64) * (HD * 17 + 32) * 4;   // merge states
+  static constexpr int BYTES = KV_BYTES > ST_BYTES ? KV_BYTES : ST_BYTES;
   static constexpr int UNITS = 2 * 64 * HD * ESZ / 16;             // uint4 per sub-tile (K + V)
   static constexpr int PER = (NSUB * UNITS + ATT_THREADS - 1) / ATT_THREADS;
 };
 
-template <int DT, int HD>
+// Split attention.  Workgroup (KV head g, split sp, query-tile group) stages
+// the split's keys and values (positions sp*256 .. sp*256+255, four 64-key
+// sub-tiles) in LDS with one batch of loads; each wave then takes one tile of
+// 16 query columns (query heads of group g x block rows) and computes, over
+// the whole split, m = max scaled score, l = sum 2^(s-m) and o = sum 2^(s-m) v
+// in a fixed order (sub-tile, key tile, key), stored for attn_combine_kernel.
+// A column's arithmetic depends only on the key positions, never on T or on
+// which workgroup ran it; keys it cannot see contribute exact zeros.
+template <int DT, int HD, bool TREE>
 __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   using LY = AttnLds<DT, HD>;
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
@@ -496,10 +533,12 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   unsigned char* Kall = lds;
   unsigned char* Vall = lds + NSUB * LY::KSUB;
 
-  const int sp = blockIdx.x, gkv = blockIdx.y, qgrp = blockIdx.z;
+  const int gkv = blockIdx.x, sp = blockIdx.y, qgrp = blockIdx.z;
+  if (sp >= a.info[1]) return;          // the grid covers the longest context
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, c = lane & 15;
-  const int nkeys = a.n + a.T;          // slots written so far
+  const int n = a.info[0];
+  const int nkeys = n + a.T;            // slots written so far
   const int base0 = sp * SPLIT;
   const int nsub = min(NSUB, (nkeys - base0 + 63) / 64);
 
@@ -508,6 +547,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
     const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
     const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
     constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
+    int pg[NSUB];
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st) pg[st] = st < nsub ? a.ptable[(base0 >> 6) + st] : 0;
     uint4 tmp[LY::PER];
     unsigned dst[LY::PER];
 #pragma unroll
@@ -519,7 +561,9 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
       dst[j] = 0xffffffffu;
       if (st < nsub) {
         const int base = base0 + st * 64;
-        const int page = a.ptable[base >> 6];
+        int page = pg[0];
+#pragma unroll
+        for (int q = 1; q < NSUB; ++q) page = st == q ? pg[q] : page;
         const int valid = nkeys - base;
         off = (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ + (size_t)u * 16);
         if (kv == 0) {
@@ -539,23 +583,21 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
       if (dst[j] == 0xffffffffu) continue;
       unsigned d = dst[j];
       uint4 v = tmp[j];
-      if (d >= (unsigned)(NSUB * LY::KSUB) && (d >> 24) != 0) {
-        // V^T chunk: zero the key columns beyond the written slots
+      if ((d >> 24) != 0) {
+        // V^T chunk: zero the key columns of unwritten slots
         const int valid = (int)(d >> 24);
         d &= 0x00ffffffu;
         if (valid < 64) {
           const int col0 = (((d - NSUB * LY::KSUB) % LY::VSUB) % VROW) / ESZ;
+          uint32_t w4[4] = {v.x, v.y, v.z, v.w};
           if (DT == DT_BF16) {
-            uint32_t w4[4] = {v.x, v.y, v.z, v.w};
             for (int e = 0; e < 8; ++e)
               if (col0 + e >= valid) w4[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-            v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
           } else {
-            if (col0 + 0 >= valid) v.x = 0;
-            if (col0 + 1 >= valid) v.y = 0;
-            if (col0 + 2 >= valid) v.z = 0;
-            if (col0 + 3 >= valid) v.w = 0;
+            for (int e = 0; e < 4; ++e)
+              if (col0 + e >= valid) w4[e] = 0;
           }
+          v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
         }
       }
       *reinterpret_cast<uint4*>(lds + d) = v;
@@ -563,90 +605,83 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   }
   __syncthreads();
 
+  // wave -> (query tile of this workgroup, sub-tile of the split)
   const int nqt = (a.ncols + 15) / 16;
-  const int qt = qgrp * a.wpg + wv;
-  if (wv >= a.wpg || qt >= nqt) return;   // no barrier follows
-
+  const int qi = wv / NSUB, st = wv % NSUB;
+  const int qt = qgrp * ATT_QT + qi;
+  const bool work = qt < nqt && st < nsub;     // uniform per wave
   const int qc = qt * 16 + c;
   const bool colok = qc < a.ncols;
   const int t = colok ? qc / a.G : 0;
   const int head = gkv * a.G + (colok ? qc % a.G : 0);
   const int mypos = colok ? a.pos[t] : -1;
-  const unsigned long long myanc = (colok && a.tree) ? a.anc[t] : 0ull;
+  const unsigned long long myanc = (TREE && colok) ? a.anc[t] : 0ull;
 
-  // query fragments (B operand): column qc, head dims [s*KS + grp*EPL, +EPL)
-  uint4 qf[NS];
-  {
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[ND];
+#pragma unroll
+  for (int i = 0; i < ND; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (work) {
+    // query fragments (B operand): column qc, head dims [s*KS + grp*EPL, +EPL)
+    uint4 qf[NS];
     const unsigned char* qb =
         reinterpret_cast<const unsigned char*>(a.q) + ((size_t)t * a.H + head) * ROWB;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       qf[s] = colok ? *reinterpret_cast<const uint4*>(qb + (s * KS + grp * EPL) * ESZ)
                     : make_uint4(0, 0, 0, 0);
-  }
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 o_run[ND];
-#pragma unroll
-  for (int i = 0; i < ND; ++i) o_run[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  for (int st = 0; st < nsub; ++st) {
-    const int base = base0 + st * 64;
     const unsigned char* Ks = Kall + st * LY::KSUB;
     const unsigned char* Vt = Vall + st * LY::VSUB;
-    // S^T = K Q^T for 4 key tiles of 16: lane holds key 16kt + 4grp + r, column c
+    const int base = base0 + st * 64;
+    // S^T = K Q^T: lane holds key 16kt + 4grp + r of column c (head-dim step
+    // outermost so consecutive MFMAs feed independent accumulators)
     f32x4 sacc[4];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < 4; ++kt) sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const uint4 kf = *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW +
-                                                         (s * KS + grp * EPL) * ESZ);
-        sacc[kt] = mma<DT>(kf, qf[s], sacc[kt]);
-      }
+    for (int s = 0; s < NS; ++s) {
+      uint4 kf[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+        kf[kt] = *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) sacc[kt] = mma<DT>(kf[kt], qf[s], sacc[kt]);
     }
-    float sv[4][4];
-    float m_sub = -INFINITY;
+    // visibility: linear rows see positions <= their own; tree rows see the
+    // committed keys, the pending row and their ancestors (bit r-1 of anc)
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int kp = base + 16 * kt + 4 * grp + r;
         bool vis;
-        if (!a.tree) {
+        if (!TREE) {
           vis = kp <= mypos;
         } else {
-          const int br = kp - a.n;   // block row held by this slot
-          vis = colok && ((kp < a.n) || br == 0 ||
-                          (br >= 1 && br < a.T && ((myanc >> (br - 1)) & 1ull)));
+          const int br = kp - n;           // block row held by this slot
+          const unsigned sh = (unsigned)(br - 1) & 63u;
+          const bool in_anc = (br >= 1) & (br < a.T) & (((myanc >> sh) & 1ull) != 0ull);
+          vis = colok & ((kp < n) | (br == 0) | in_anc);
         }
         const float x = vis ? sacc[kt][r] * a.scale_log2 : -INFINITY;
-        sv[kt][r] = x;
-        m_sub = fmaxf(m_sub, x);
+        sacc[kt][r] = x;
+        m = fmaxf(m, x);
       }
-    m_sub = fmaxf(m_sub, __shfl_xor(m_sub, 16));
-    m_sub = fmaxf(m_sub, __shfl_xor(m_sub, 32));
-    const float m_new = fmaxf(m_run, m_sub);
-    const bool any = m_new != -INFINITY;
-    const float alpha = (any && m_run != -INFINITY) ? exp2f(m_run - m_new) : (any ? 0.f : 1.f);
-    float p[4][4];
-    float l_sub = 0.f;
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const float m_use = m != -INFINITY ? m : 0.f;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        p[kt][r] = any ? exp2f(sv[kt][r] - m_new) : 0.f;
-        l_sub += p[kt][r];
+        const float pv = exp2f(sacc[kt][r] - m_use);   // exp2(-inf) = 0 for hidden keys
+        sacc[kt][r] = pv;
+        l += pv;
       }
-    l_sub += __shfl_xor(l_sub, 16);
-    l_sub += __shfl_xor(l_sub, 32);
-    l_run = l_run * alpha + l_sub;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < ND; ++i) o_run[i] *= alpha;
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
 
-    // O^T += V^T P^T; reduction over the 64 keys of the sub-tile
+    // O^T = V^T P^T over the sub-tile's 64 keys
     if (DT == DT_BF16) {
       // P enters the bf16 MFMA as hi + lo bf16 parts (about 16 significant
       // bits), so the weights of the value rows keep near-fp32 precision.
@@ -655,49 +690,90 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
         uint32_t ph[8], pl[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float pv = p[2 * k2 + (e >> 2)][e & 3];
-          ph[e] = f2bf_bits(pv);
-          pl[e] = f2bf_bits(pv - bf2f(ph[e]));
+          const float pv = sacc[2 * k2 + (e >> 2)][e & 3];
+          ph[e] = f2bf_bits_finite(pv);
+          pl[e] = f2bf_bits_finite(pv - bf2f(ph[e]));
         }
         const uint4 pfh = make_uint4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
                                      ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16));
         const uint4 pfl = make_uint4(pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
                                      pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16));
+        uint4 vf[ND];
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
           const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
           const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * k2 + 4 * grp) * ESZ);
           const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * k2 + 16 + 4 * grp) * ESZ);
-          const uint4 vf = make_uint4(lo.x, lo.y, hi.x, hi.y);
-          o_run[dt] = mma<DT>(vf, pfh, o_run[dt]);
-          o_run[dt] = mma<DT>(vf, pfl, o_run[dt]);
+          vf[dt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
         }
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfh, o[dt]);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfl, o[dt]);
       }
     } else {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const uint4 pf = make_uint4(__float_as_uint(p[kt][0]), __float_as_uint(p[kt][1]),
-                                    __float_as_uint(p[kt][2]), __float_as_uint(p[kt][3]));
+        const uint4 pf = make_uint4(__float_as_uint(sacc[kt][0]), __float_as_uint(sacc[kt][1]),
+                                    __float_as_uint(sacc[kt][2]), __float_as_uint(sacc[kt][3]));
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
           const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
           const uint4 vf = *reinterpret_cast<const uint4*>(vr + (16 * kt + 4 * grp) * ESZ);
-          o_run[dt] = mma<DT>(vf, pf, o_run[dt]);
+          o[dt] = mma<DT>(vf, pf, o[dt]);
         }
       }
     }
   }
 
-  if (colok) {
-    float* out = a.part + (((size_t)sp * a.Hkv + gkv) * a.ncols + qc) * (HD + 2);
+  // sub-tile states -> LDS (over the staged keys, no longer needed); merge in
+  // sub-tile order: M = max m, w = 2^(m - M), L = sum l w, O = sum o w
+  __syncthreads();
+  float* stO = reinterpret_cast<float*>(lds);                          // [ATT_QT][NSUB][HD][17]
+  float* stM = stO + ATT_QT * NSUB * HD * 17;                           // [ATT_QT][NSUB][16]
+  float* stL = stM + ATT_QT * NSUB * 16;
+  {
+    float* so = stO + ((size_t)(qi * NSUB + st) * HD) * 17;
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) out[16 * dt + 4 * grp + r] = o_run[dt][r];
+      for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = o[dt][r];
     if (grp == 0) {
-      out[HD] = m_run;
-      out[HD + 1] = l_run;
+      stM[(qi * NSUB + st) * 16 + c] = m;
+      stL[(qi * NSUB + st) * 16 + c] = l;
     }
+  }
+  __syncthreads();
+  // thread -> (query tile, column, HD/16 dims)
+  constexpr int DPT = HD / 16;
+  const int mq = threadIdx.x / 256, rest = threadIdx.x % 256;
+  const int col = rest & 15, d0 = (rest >> 4) * DPT;
+  const int qcol = (qgrp * ATT_QT + mq) * 16 + col;
+  if (qcol >= a.ncols) return;
+  float M = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < NSUB; ++j)
+    if (stL[(mq * NSUB + j) * 16 + col] > 0.f) M = fmaxf(M, stM[(mq * NSUB + j) * 16 + col]);
+  float L = 0.f, O[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) O[e] = 0.f;
+#pragma unroll
+  for (int j = 0; j < NSUB; ++j) {
+    const float lj = stL[(mq * NSUB + j) * 16 + col];
+    if (!(lj > 0.f)) continue;
+    const float w = exp2f(stM[(mq * NSUB + j) * 16 + col] - M);
+    L = fmaf(lj, w, L);
+    const float* so = stO + ((size_t)(mq * NSUB + j) * HD + d0) * 17 + col;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) O[e] = fmaf(so[e * 17], w, O[e]);
+  }
+  float* out = a.part + (((size_t)sp * a.Hkv + gkv) * a.ncols + qcol) * (HD + 2);
+#pragma unroll
+  for (int e = 0; e < DPT; e += 4)
+    *reinterpret_cast<float4*>(out + d0 + e) = make_float4(O[e], O[e + 1], O[e + 2], O[e + 3]);
+  if (d0 == 0) {
+    out[HD] = M;
+    out[HD + 1] = L;
   }
 }
 
@@ -706,9 +782,11 @@ constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 // Merge the splits of every (row, head) in split order; write the attention
 // output as packed activations of the O projection.  4 dims per thread.
 template <int DT, int HD>
-__global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part, int nsplit,
+__global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part,
+                                                              const int* __restrict__ info,
                                                               int Hkv, int G, int ncols, int H,
                                                               void* __restrict__ xout, int x_S) {
+  const int nsplit = info[1];
   const int t = blockIdx.x / H, j = blockIdx.x % H;
   const int gkv = j / G, qc = t * G + (j % G);
   const int dim = threadIdx.x * 4;
@@ -819,8 +897,10 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
 template <int DT, int HD>
 __global__ __launch_bounds__(256) void compact_kernel(void* __restrict__ kv_pool, size_t layer_stride,
                                                       const int* __restrict__ ptable,
-                                                      const int* __restrict__ result, int n, int Hkv) {
+                                                      const int* __restrict__ result,
+                                                      const int* __restrict__ info, int Hkv) {
   constexpr int ESZ = Geo<DT>::ESZ;
+  const int n = info[0];
   const int layer = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
   const int a = result[0];
   unsigned char* lb = reinterpret_cast<unsigned char*>(kv_pool) + layer * layer_stride * ESZ;
@@ -890,11 +970,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     return e;
 
   const int G = m.H / m.Hkv, ncols = T * G;
-  const int nkeys = s.n + T;
-  const int nsplit = (nkeys + SPLIT - 1) / SPLIT;
+  const int nsplit = w.max_splits;   // splits beyond the context exit at once
   const int nqt = (ncols + 15) / 16;
-  const int nqg = (nqt + 15) / 16;
-  const int wpb = (nqt + nqg - 1) / nqg;   // q-tiles per workgroup (<= 16 waves)
   const int pairs = (m.H + 2 * m.Hkv) * (m.hd / 2);
 
   for (int l = 0; l < m.L; ++l) {
@@ -905,27 +982,32 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
            hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, T), dim3(256), 0, st, w.part,
-                              sk_d, T, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.ptable, s.n, w.q, kvl);
+                              sk_d, T, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.ptable, w.info, w.q, kvl);
            return last();
          })) != hipSuccess)
       return e;
     // attention
     AttnArgs aa{};
     aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.anc = w.anc;
-    aa.T = T; aa.n = s.n; aa.H = m.H; aa.Hkv = m.Hkv; aa.G = G; aa.ncols = ncols;
+    aa.info = w.info;
+    aa.T = T; aa.H = m.H; aa.Hkv = m.Hkv; aa.G = G; aa.ncols = ncols;
     aa.tree = s.mode == 2;
     aa.scale_log2 = 1.4426950408889634f / sqrtf((float)m.hd);
     aa.part = w.attn_part;
     aa.max_pages = m.max_pages;
-    aa.wpg = wpb;
     if ((e = timed(prof, PC_ATTN, st, [&] {
-           hipLaunchKernelGGL((attn_kernel<DT, HD>), dim3(nsplit, m.Hkv, nqg), dim3(ATT_THREADS), 0, st, aa);
+           // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
+           const dim3 grid(m.Hkv, nsplit, (nqt + ATT_QT - 1) / ATT_QT);
+           if (aa.tree)
+             hipLaunchKernelGGL((attn_kernel<DT, HD, true>), grid, dim3(ATT_THREADS), 0, st, aa);
+           else
+             hipLaunchKernelGGL((attn_kernel<DT, HD, false>), grid, dim3(ATT_THREADS), 0, st, aa);
            return last();
          })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
            hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(T * m.H), dim3(HD / 4), 0, st, w.attn_part,
-                              nsplit, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
+                              w.info, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
       return e;
@@ -995,11 +1077,11 @@ hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof,
   const dim3 grid(m.L * m.Hkv), block(256);
   return timed(prof, PC_COMPACT, st, [&] {
     if (m.dt == DT_BF16 && m.hd == 128)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, s.n, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
     else if (m.dt == DT_BF16 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, s.n, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
     else if (m.dt == DT_F32 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, s.n, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
     else
       return hipErrorInvalidValue;   // fp32 with head_dim 128 would exceed the LDS staging size
     return hipGetLastError();

@@ -73,3 +73,30 @@ def test_row_logits_independent_of_block_size(ee):
         assert a == k and nxt == toks[k + 1]
         np.testing.assert_array_equal(eng.logits(), np.stack(ar_rows[:k + 1]))
     eng.close()
+
+
+def test_graph_replays_equal_eager_launches(ee):
+    """Every replay of a captured block graph gives the eager result bitwise,
+    with eager work and synchronisations between the replays."""
+    import torch
+    shape = get_shape("tiny", n_layers=2, d_model=512, n_heads=4, n_kv_heads=2, head_dim=128,
+                      ffn=1024, vocab=2048, dtype="bf16")
+    w = gen_weights(shape, seed=8, std=0.05)
+    prompt = zipf_tokens(shape.vocab, 100, seed=3)
+    draft = zipf_tokens(shape.vocab, 20, seed=4)
+    eng = ee.Engine(shape, w, max_ctx=512, k_max=32)
+    first = eng.prefill(0, prompt)
+    n0 = eng.seq_state(0)[0]
+    eng.use_graphs(False)
+    ref = eng.verify(0, draft)
+    ref_logits = eng.logits()
+    eng.use_graphs(True)
+    for rep in range(4):
+        eng.rollback(0, n0, first)
+        x = torch.randn(1 << 20, device="cuda") * 2.0      # unrelated eager work
+        torch.cuda.synchronize()
+        got = eng.verify(0, draft)
+        assert got[:2] == ref[:2]
+        np.testing.assert_array_equal(eng.logits(), ref_logits)
+        del x
+    eng.close()
