@@ -63,6 +63,23 @@ def gateup_bytes(s, t: int) -> int:
     return esz * (2 * s.ffn * s.d_model + t * s.d_model)
 
 
+def measured_traffic():
+    """Per-launch HBM bytes of the gate/up GEMM from the committed counter
+    summary, or None if the kernel source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_gateup_7b_k32_traffic.md")
+    src = os.path.join(ROOT, "paper_2506_02780_amd", "csrc", "kernels.hip")
+    try:
+        text = open(path).read()
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    fields = dict(ln.split(": ", 1) for ln in text.splitlines() if ": " in ln and ln[:1].isalpha())
+    if fields.get("kernels_hip_sha256", "").strip() != digest:
+        return None
+    return int(fields["gateup_traffic_bytes_per_launch"])
+
+
 def cpu_baseline(shape, weights, k: int, ctx: int, layers: int, emitted_per_step: float):
     """Time the oracle on a bounded sample of one verify step and scale it."""
     from threadpoolctl import threadpool_info
@@ -119,6 +136,7 @@ def main():
     ap.add_argument("--gen", type=int, default=512, help="length of the greedy output re-created")
     ap.add_argument("--cpu-layers", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -140,6 +158,8 @@ def main():
     log(f"[bench] weights drawn in {time.perf_counter() - t0:.1f}s")
     max_ctx = ctx + args.gen + K + 2
     eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=max(K, 1))
+    if args.eager:
+        eng.use_graphs(False)
     log(f"[bench] engine ready at {time.perf_counter() - t0:.1f}s")
 
     prompt = zipf_tokens(shape.vocab, ctx, seed=42)
@@ -214,6 +234,14 @@ def main():
     p90 = float(np.percentile(fixed, 90))
     sb = step_bytes(shape, T, ctx)
 
+    # a plain device copy of known size, so that hardware byte counters read on
+    # this run can be scaled against it
+    cal = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+    cal_dst = torch.empty_like(cal)
+    cal_dst.copy_(cal)
+    torch.cuda.synchronize()
+    del cal, cal_dst
+
     # per-class breakdown of one step (separate pass, every class instrumented)
     eng.profile(list(ee.PROF_CLASSES))
     for _ in range(10):
@@ -254,7 +282,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gu_alg / gu_avg_s / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
             "launch_us": round(gu_avg_s * 1e6, 2),
             "launches": int(gu_n),
             "bytes_per_launch": gu_alg,
