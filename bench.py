@@ -63,19 +63,33 @@ def gateup_bytes(s, t: int) -> int:
     return esz * (2 * s.ffn * s.d_model + t * s.d_model)
 
 
+def _gemm_source_digest(path):
+    """sha256 of the GEMM section of the kernel source (from its section
+    banner to the next one): the code the counter figures were taken on."""
+    import hashlib
+    out, on = [], False
+    for ln in open(path).read().splitlines(keepends=True):
+        if ln.startswith("// ----"):
+            if on:
+                break
+            on = ln.rstrip().endswith(" GEMM --")
+        if on:
+            out.append(ln)
+    return hashlib.sha256("".join(out).encode()).hexdigest() if out else None
+
+
 def measured_traffic():
     """Per-launch HBM bytes of the gate/up GEMM from the committed counter
-    summary, or None if the kernel source has changed since it was taken."""
-    import hashlib
+    summary, or None if the GEMM source has changed since it was taken."""
     path = os.path.join(ROOT, "profiles", "gemm_gateup_7b_k32_traffic.md")
     src = os.path.join(ROOT, "paper_2506_02780_amd", "csrc", "kernels.hip")
     try:
         text = open(path).read()
-        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        digest = _gemm_source_digest(src)
     except OSError:
         return None
     fields = dict(ln.split(": ", 1) for ln in text.splitlines() if ": " in ln and ln[:1].isalpha())
-    if fields.get("kernels_hip_sha256", "").strip() != digest:
+    if digest is None or fields.get("gemm_source_sha256", "").strip() != digest:
         return None
     return int(fields["gateup_traffic_bytes_per_launch"])
 
@@ -275,7 +289,7 @@ def main():
         "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4)},
         "roofline": {
-            "kernel": "gemm_kernel<bf16, MT=3> (gate/up projection, T=33)",
+            "kernel": f"gemm_kernel<{shape.dtype}, MT={(T + 15) // 16}> (gate/up projection, T={T})",
             "measured": "HIP events around each gate/up launch over a second run of the timed workload",
             "bound": "hbm",
             "achieved": round(gu_alg / gu_avg_s / 1e9, 1),

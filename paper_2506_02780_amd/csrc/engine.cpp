@@ -43,7 +43,7 @@ struct Layout {
   // workspace
   size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
-  size_t s_tok, s_pos, s_prow, s_anc, s_ptable, s_info, stage_bytes;
+  size_t s_tok, s_pos, s_prow, s_path, s_ptable, s_info, stage_bytes;
   size_t kv_layer, kv_total;
 };
 
@@ -69,6 +69,12 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0");
   if ((c->n_heads / c->n_kv_heads) * (c->k_max + 1) > 64 * 16 * 16)
     return bad("too many query columns per KV head");
+  {
+    // one layer of the KV pool is addressed with 32-bit buffer offsets
+    const size_t pages = (size_t)((c->max_ctx + PAGE - 1) / PAGE) * c->max_seqs;
+    const size_t layer = pages * 2 * c->n_kv_heads * PAGE * c->head_dim * (c->dtype == EE_BF16 ? 2 : 4);
+    if (layer >= (size_t(1) << 31)) return bad("one layer of the KV pool must stay below 2 GiB");
+  }
   return true;
 }
 
@@ -127,10 +133,10 @@ Layout make_layout(const ee_model_config* c) {
   L.result = o; o += up((2 + 64) * 4);
   // staging block: one host->device copy per call
   size_t so = 0;
-  L.s_anc = so; so += L.Tmax * 8;
   L.s_tok = so; so += L.Tmax * 4;
   L.s_pos = so; so += L.Tmax * 4;
   L.s_prow = so; so += L.Tmax * 4;
+  L.s_path = so; so += L.Tmax * 64;
   L.s_ptable = so; so += L.pages_per_seq * 4;
   L.s_info = so; so += 4 * 4;
   L.stage_bytes = up(so);
@@ -211,7 +217,7 @@ void bind_work(ee_ctx* c) {
   w.greedy = reinterpret_cast<int*>(ws + L.greedy);
   w.result = reinterpret_cast<int*>(ws + L.result);
   unsigned char* sb = ws + L.stage;
-  w.anc = reinterpret_cast<unsigned long long*>(sb + L.s_anc);
+  w.path = sb + L.s_path;
   w.tok = reinterpret_cast<int*>(sb + L.s_tok);
   w.pos = reinterpret_cast<int*>(sb + L.s_pos);
   w.prow = reinterpret_cast<int*>(sb + L.s_prow);
@@ -526,7 +532,7 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
   int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
   int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
-  unsigned long long* anc = reinterpret_cast<unsigned long long*>(c->h_stage + L.s_anc);
+  unsigned char* path = c->h_stage + L.s_path;
   int depth[65];
   if (parent) {
     depth[0] = 0;
@@ -541,18 +547,16 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   tok[0] = s.pending;
   pos[0] = s.len;
   prow[0] = -1;
-  anc[0] = 0;
   for (int r = 1; r < T; ++r) {
     tok[r] = draft[r - 1];
     if (parent) {
-      const int pr = parent[r - 1] + 1;
-      prow[r] = pr;
+      prow[r] = parent[r - 1] + 1;
       pos[r] = s.len + depth[r];
-      anc[r] = (pr >= 1 ? anc[pr] : 0ull) | (1ull << (r - 1));
+      // the rows on r's path, by depth (attention sees them at n+1 .. n+depth)
+      for (int x = r, j = depth[r]; x >= 1; x = prow[x], --j) path[r * 64 + j - 1] = (unsigned char)x;
     } else {
       prow[r] = r - 1;
       pos[r] = s.len + r;
-      anc[r] = (r >= 2 ? anc[r - 1] : 0ull) | (1ull << (r - 1));
     }
   }
   rc = run_block(c, s, T, parent ? 2 : 1);

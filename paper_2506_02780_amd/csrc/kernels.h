@@ -72,8 +72,8 @@ struct Work {
   int* tok;                 // [Tmax]
   int* pos;                 // [Tmax] rotary position of each row
   int* prow;                // [Tmax] parent row (tree) or r-1
-  unsigned long long* anc;  // [Tmax] bit c-1: block row c >= 1 is an ancestor-or-self
-                            // (row 0, the pending token, is seen by every row)
+  unsigned char* path;      // [Tmax][64] tree mode: entry j-1 of row t = block row at
+                            // depth j on t's path (row 0, the pending token, is depth 0)
   int* ptable;              // [max_pages] page of each 64-position block
   int* info;                // [0] committed positions n, [1] attention splits in use
   int max_splits;           // attention splits of the longest context

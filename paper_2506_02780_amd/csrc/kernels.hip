@@ -479,7 +479,7 @@ struct AttnArgs {
   const void* kv_layer;     // [pages][2][Hkv][64*hd]
   const int* ptable;
   const int* pos;
-  const unsigned long long* anc;
+  const unsigned char* path;  // tree: [T][64], entry j-1 = block row at depth j on row t's path
   const int* info;          // [0] committed positions n, [1] splits in use
   int T, H, Hkv, G, ncols;
   int tree;
@@ -513,6 +513,104 @@ template <int DT, int HD> struct AttnLds {
   static constexpr int UNITS = 2 * 64 * HD * ESZ / 16;             // uint4 per sub-tile (K + V)
   static constexpr int PER = (NSUB * UNITS + ATT_THREADS - 1) / ATT_THREADS;
 };
+
+// One 64-key sub-tile for the wave's 16 query columns: scores S^T = K Q^T
+// (head-dim step outermost, so consecutive MFMAs feed independent
+// accumulators), m = max visible scaled score, l = sum 2^(s-m) and
+// o = sum 2^(s-m) v.  kfn(kt, s) gives the key fragment of key 16kt + c at head
+// dims s*KS + grp*EPL ..; vfn(dt, j) the value fragment of output dims 16dt + c
+// (bf16, j = k2: keys 32j + 4grp + 0..3 then 32j + 16 + 4grp + 0..3; fp32,
+// j = kt: keys 16j + 4grp + 0..3).  Key 16kt + 4grp + r of the sub-tile sits at
+// position base + 16kt + 4grp + r and is visible to a column iff that position
+// is <= the column's own.  A column's result depends only on its query, the
+// key/value data and the positions, never on the other columns.  o is
+// accumulated into (the caller clears it); columns with own == false add
+// exact zeros to it.  STREAMV fetches each value fragment right before its
+// MFMAs (fewer live registers; the same arithmetic in the same order).
+template <int DT, int HD, bool STREAMV, class KFn, class VFn>
+__device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, VFn vfn, int base,
+                                              int mypos, float scale_log2, int grp, bool own, float& m,
+                                              float& l, f32x4 (&o)[HD / 16]) {
+  constexpr int NS = HD / Geo<DT>::KS, ND = HD / 16;
+  f32x4 sacc[4];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    uint4 kf[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) kf[kt] = kfn(kt, s);
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) sacc[kt] = mma<DT>(kf[kt], qf[s], sacc[kt]);
+  }
+  m = -INFINITY;
+  l = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int kp = base + 16 * kt + 4 * grp + r;
+      const float x = kp <= mypos ? sacc[kt][r] * scale_log2 : -INFINITY;
+      sacc[kt][r] = x;
+      m = fmaxf(m, x);
+    }
+  m = fmaxf(m, __shfl_xor(m, 16));
+  m = fmaxf(m, __shfl_xor(m, 32));
+  const float m_use = m != -INFINITY ? m : 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float pv = exp2f(sacc[kt][r] - m_use);   // exp2(-inf) = 0 for hidden keys
+      sacc[kt][r] = own ? pv : 0.f;
+      l += pv;
+    }
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  // O^T = V^T P^T over the sub-tile's 64 keys
+  if (DT == DT_BF16) {
+    // P enters the bf16 MFMA as hi + lo bf16 parts (about 16 significant
+    // bits), so the weights of the value rows keep near-fp32 precision.
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      uint32_t ph[8], pl[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float pv = sacc[2 * k2 + (e >> 2)][e & 3];
+        ph[e] = f2bf_bits_finite(pv);
+        pl[e] = f2bf_bits_finite(pv - bf2f(ph[e]));
+      }
+      const uint4 pfh = make_uint4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
+                                   ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16));
+      const uint4 pfl = make_uint4(pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
+                                   pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16));
+      if (STREAMV) {
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+          const uint4 vf = vfn(dt, k2);
+          o[dt] = mma<DT>(vf, pfh, o[dt]);
+          o[dt] = mma<DT>(vf, pfl, o[dt]);
+        }
+      } else {
+        uint4 vf[ND];
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) vf[dt] = vfn(dt, k2);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfh, o[dt]);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfl, o[dt]);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      const uint4 pf = make_uint4(__float_as_uint(sacc[kt][0]), __float_as_uint(sacc[kt][1]),
+                                  __float_as_uint(sacc[kt][2]), __float_as_uint(sacc[kt][3]));
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vfn(dt, kt), pf, o[dt]);
+    }
+  }
+}
 
 // Split attention.  Workgroup (KV head g, split sp, query-tile group) stages
 // the split's keys and values (positions sp*256 .. sp*256+255, four 64-key
@@ -615,7 +713,7 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   const int t = colok ? qc / a.G : 0;
   const int head = gkv * a.G + (colok ? qc % a.G : 0);
   const int mypos = colok ? a.pos[t] : -1;
-  const unsigned long long myanc = (TREE && colok) ? a.anc[t] : 0ull;
+  const int base = base0 + st * 64;
 
   float m = -INFINITY, l = 0.f;
   f32x4 o[ND];
@@ -630,97 +728,97 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
     for (int s = 0; s < NS; ++s)
       qf[s] = colok ? *reinterpret_cast<const uint4*>(qb + (s * KS + grp * EPL) * ESZ)
                     : make_uint4(0, 0, 0, 0);
-    const unsigned char* Ks = Kall + st * LY::KSUB;
-    const unsigned char* Vt = Vall + st * LY::VSUB;
-    const int base = base0 + st * 64;
-    // S^T = K Q^T: lane holds key 16kt + 4grp + r of column c (head-dim step
-    // outermost so consecutive MFMAs feed independent accumulators)
-    f32x4 sacc[4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      uint4 kf[4];
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-        kf[kt] = *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) sacc[kt] = mma<DT>(kf[kt], qf[s], sacc[kt]);
+    // A tree row at depth j sits at position n + j and sees, at positions
+    // n+1 .. n+j, its ancestors in depth order: exactly what the chain along
+    // its path would hold there.  Sub-tiles reaching those positions are
+    // computed once per block row of the tile, from keys and values gathered
+    // by position; every other sub-tile holds committed keys and the pending
+    // row only, the same for every row, and is read from the staged image.
+    bool gather = false;
+    if (TREE) {
+      int mx = mypos;
+      mx = max(mx, __shfl_xor(mx, 1));
+      mx = max(mx, __shfl_xor(mx, 2));
+      mx = max(mx, __shfl_xor(mx, 4));
+      mx = max(mx, __shfl_xor(mx, 8));
+      gather = mx > n && base + 63 > n && base <= mx;   // uniform: mx is a wave maximum
     }
-    // visibility: linear rows see positions <= their own; tree rows see the
-    // committed keys, the pending row and their ancestors (bit r-1 of anc)
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kp = base + 16 * kt + 4 * grp + r;
-        bool vis;
-        if (!TREE) {
-          vis = kp <= mypos;
-        } else {
-          const int br = kp - n;           // block row held by this slot
-          const unsigned sh = (unsigned)(br - 1) & 63u;
-          const bool in_anc = (br >= 1) & (br < a.T) & (((myanc >> sh) & 1ull) != 0ull);
-          vis = colok & ((kp < n) | (br == 0) | in_anc);
+    if (!gather) {
+      const unsigned char* Ks = Kall + st * LY::KSUB;
+      const unsigned char* Vt = Vall + st * LY::VSUB;
+      auto kfn = [&](int kt, int s) {
+        return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+      };
+      auto vfn = [&](int dt, int j) {
+        const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
+        if (DT == DT_BF16) {
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
+          return make_uint4(lo.x, lo.y, hi.x, hi.y);
         }
-        const float x = vis ? sacc[kt][r] * a.scale_log2 : -INFINITY;
-        sacc[kt][r] = x;
-        m = fmaxf(m, x);
-      }
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    const float m_use = m != -INFINITY ? m : 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pv = exp2f(sacc[kt][r] - m_use);   // exp2(-inf) = 0 for hidden keys
-        sacc[kt][r] = pv;
-        l += pv;
-      }
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-
-    // O^T = V^T P^T over the sub-tile's 64 keys
-    if (DT == DT_BF16) {
-      // P enters the bf16 MFMA as hi + lo bf16 parts (about 16 significant
-      // bits), so the weights of the value rows keep near-fp32 precision.
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        uint32_t ph[8], pl[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = sacc[2 * k2 + (e >> 2)][e & 3];
-          ph[e] = f2bf_bits_finite(pv);
-          pl[e] = f2bf_bits_finite(pv - bf2f(ph[e]));
-        }
-        const uint4 pfh = make_uint4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
-                                     ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16));
-        const uint4 pfl = make_uint4(pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
-                                     pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16));
-        uint4 vf[ND];
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) {
-          const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * k2 + 4 * grp) * ESZ);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * k2 + 16 + 4 * grp) * ESZ);
-          vf[dt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfh, o[dt]);
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[dt] = mma<DT>(vf[dt], pfl, o[dt]);
-      }
+        return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
+      };
+      subtile_state<DT, HD, false>(qf, kfn, vfn, base, mypos, a.scale_log2, grp, true, m, l, o);
     } else {
+      const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
+      const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
+      const int t_lo = (qt * 16) / a.G, t_hi = (min(qt * 16 + 15, a.ncols - 1)) / a.G;
+      for (int tr = t_lo; tr <= t_hi; ++tr) {
+        const int dep = a.pos[tr] - n;
+        // physical slot holding position kp on row tr's path (-1: hidden)
+        auto slot_of = [&](int kp) {
+          if (kp <= n) return kp;
+          return kp - n <= dep ? n + (int)a.path[tr * 64 + (kp - n - 1)] : -1;
+        };
+        // byte offset of slot ps's K row (kv = 0) or V^T column (kv = 1)
+        auto off_of = [&](int ps, int kv) {
+          if (ps < 0) return OOB;
+          const int page = a.ptable[ps >> 6];
+          return (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ +
+                            (size_t)(ps & 63) * (kv ? 1 : HD) * ESZ);
+        };
+        unsigned koff[4];
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        const uint4 pf = make_uint4(__float_as_uint(sacc[kt][0]), __float_as_uint(sacc[kt][1]),
-                                    __float_as_uint(sacc[kt][2]), __float_as_uint(sacc[kt][3]));
+        for (int kt = 0; kt < 4; ++kt) koff[kt] = off_of(slot_of(base + 16 * kt + c), 0);
+        constexpr int NVK = 16;                      // value keys held per lane
+        unsigned voff[NVK];
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) {
-          const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-          const uint4 vf = *reinterpret_cast<const uint4*>(vr + (16 * kt + 4 * grp) * ESZ);
-          o[dt] = mma<DT>(vf, pf, o[dt]);
+        for (int i = 0; i < NVK; ++i) {
+          // bf16: key 32(i/8) + 16((i%8)/4) + 4grp + i%4;  fp32: key 16(i/4) + 4grp + i%4
+          const int key = DT == DT_BF16 ? 32 * (i >> 3) + 16 * ((i >> 2) & 1) + 4 * grp + (i & 3)
+                                        : 16 * (i >> 2) + 4 * grp + (i & 3);
+          voff[i] = off_of(slot_of(base + key), 1);
+        }
+        auto kfn = [&](int kt, int s) {
+          return bload<0>(rs, koff[kt] == OOB ? OOB : koff[kt] + (unsigned)((s * KS + grp * EPL) * ESZ));
+        };
+        auto vfn = [&](int dt, int j) {
+          const unsigned drow = (unsigned)((16 * dt + c) * 64 * ESZ);
+          uint32_t w[4];
+          if (DT == DT_BF16) {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const int i0 = 8 * j + 2 * h;
+              const uint32_t x0 = __builtin_amdgcn_raw_buffer_load_b16(rs, voff[i0] == OOB ? OOB : voff[i0] + drow, 0, 0);
+              const uint32_t x1 = __builtin_amdgcn_raw_buffer_load_b16(rs, voff[i0 + 1] == OOB ? OOB : voff[i0 + 1] + drow, 0, 0);
+              w[h] = (x0 & 0xffffu) | (x1 << 16);
+            }
+          } else {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const int i0 = 4 * j + h;
+              w[h] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff[i0] == OOB ? OOB : voff[i0] + drow, 0, 0);
+            }
+          }
+          return make_uint4(w[0], w[1], w[2], w[3]);
+        };
+        // every column accumulates; only row tr's columns get non-zero weights
+        const bool own = colok && t == tr;
+        float mt, lt;
+        subtile_state<DT, HD, true>(qf, kfn, vfn, base, mypos, a.scale_log2, grp, own, mt, lt, o);
+        if (own) {
+          m = mt;
+          l = lt;
         }
       }
     }
@@ -988,7 +1086,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     // attention
     AttnArgs aa{};
-    aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.anc = w.anc;
+    aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.path = w.path;
     aa.info = w.info;
     aa.T = T; aa.H = m.H; aa.Hkv = m.Hkv; aa.G = G; aa.ncols = ncols;
     aa.tree = s.mode == 2;
