@@ -137,7 +137,8 @@ Layout make_layout(const ee_model_config* c) {
   L.s_pos = so; so += L.Tmax * 4;
   L.s_prow = so; so += L.Tmax * 4;
   L.s_path = so; so += L.Tmax * 64;
-  L.s_ptable = so; so += L.pages_per_seq * 4;
+  so = (so + 15) & ~(size_t)15;   // 16-byte loads of page numbers
+  L.s_ptable = so; so += ((L.pages_per_seq + 3) & ~3) * 4;
   L.s_info = so; so += 4 * 4;
   L.stage_bytes = up(so);
   L.stage = o; o += L.stage_bytes;

@@ -299,68 +299,85 @@ __device__ __forceinline__ void store8(void* xout, int t, int col, int S, const 
 
 // ------------------------------------------------------------ embed / norm --
 
-// Fixed-order block sum of one float per thread (blockDim.x == 256).
-__device__ __forceinline__ float block_sum256(float v, float* sh) {
-  sh[threadIdx.x] = v;
+constexpr int NORM_THREADS = 512;
+
+// Fixed-order sum of one float per thread over a NORM_THREADS block: an xor
+// butterfly inside each wave (every lane ends with the same bits), then the
+// wave sums in wave order.
+__device__ __forceinline__ float block_sum_norm(float v, float* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) sh[threadIdx.x] = sh[threadIdx.x] + sh[threadIdx.x + w];
-    __syncthreads();
-  }
-  const float r = sh[0];
-  __syncthreads();
+  float r = sh[0];
+#pragma unroll
+  for (int w = 1; w < NORM_THREADS / 64; ++w) r += sh[w];
   return r;
 }
 
 // Row t of the residual stream: h = E[tok[t]] (MODE 0) or h += sum of the
 // GEMM slice partials (MODE 1); then x = RMSNorm(h) * gain, packed as the
-// next GEMM's activations.  Each thread owns 8-column chunks (d % 8 == 0).
+// next GEMM's activations.  Each thread owns up to two 8-column chunks
+// (d <= 8192, d % 8 == 0); every load is issued before the first use.
 template <int DT, int MODE>
-__global__ __launch_bounds__(256) void norm_kernel(const void* __restrict__ embed,
-                                                   const int* __restrict__ tok, float* __restrict__ h,
-                                                   const float* __restrict__ part, int SK, int T,
-                                                   const float* __restrict__ gain, float eps, int d,
-                                                   void* __restrict__ xout, int x_S) {
-  __shared__ float sh[256];
+__global__ __launch_bounds__(NORM_THREADS) void norm_kernel(const void* __restrict__ embed,
+                                                            const int* __restrict__ tok, float* __restrict__ h,
+                                                            const float* __restrict__ part, int SK, int T,
+                                                            const float* __restrict__ gain, float eps, int d,
+                                                            void* __restrict__ xout, int x_S) {
+  __shared__ float sh[NORM_THREADS / 64];
   const int t = blockIdx.x;
   float* hr = h + (size_t)t * d;
   const int nch = d / 8;
-  constexpr int MAXCH = 4;               // d <= 8192
-  float v[MAXCH][8];
+  constexpr int MAXCH = 2;
+  float v[MAXCH][8], gn[MAXCH][8];
+  const int row = MODE == 0 ? tok[t] : 0;
+#pragma unroll
+  for (int j = 0; j < MAXCH; ++j) {
+    const int ch = threadIdx.x + NORM_THREADS * j;
+    if (ch < nch) {
+      const int col = ch * 8;
+      const float4 g0 = *reinterpret_cast<const float4*>(gain + col);
+      const float4 g1 = *reinterpret_cast<const float4*>(gain + col + 4);
+      gn[j][0] = g0.x; gn[j][1] = g0.y; gn[j][2] = g0.z; gn[j][3] = g0.w;
+      gn[j][4] = g1.x; gn[j][5] = g1.y; gn[j][6] = g1.z; gn[j][7] = g1.w;
+      if (MODE == 0) {
+        const size_t e0 = (size_t)row * d + col;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[j][e] = load_elt<DT>(embed, e0 + e);
+      } else {
+        const float4 h0 = *reinterpret_cast<const float4*>(hr + col);
+        const float4 h1 = *reinterpret_cast<const float4*>(hr + col + 4);
+        const float4 p0 = sum_slices4(part, SK, T, d, t, col);
+        const float4 p1 = sum_slices4(part, SK, T, d, t, col + 4);
+        v[j][0] = h0.x + p0.x; v[j][1] = h0.y + p0.y; v[j][2] = h0.z + p0.z; v[j][3] = h0.w + p0.w;
+        v[j][4] = h1.x + p1.x; v[j][5] = h1.y + p1.y; v[j][6] = h1.z + p1.z; v[j][7] = h1.w + p1.w;
+      }
+    }
+  }
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < MAXCH; ++j) {
-    const int ch = threadIdx.x + 256 * j;
-    if (ch >= nch) break;
-    const int col = ch * 8;
-    if (MODE == 0) {
-      const size_t e0 = (size_t)tok[t] * d + col;
+    const int ch = threadIdx.x + NORM_THREADS * j;
+    if (ch < nch) {
+      const int col = ch * 8;
+      *reinterpret_cast<float4*>(hr + col) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+      *reinterpret_cast<float4*>(hr + col + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[j][e] = load_elt<DT>(embed, e0 + e);
-    } else {
-      const float4 h0 = *reinterpret_cast<const float4*>(hr + col);
-      const float4 h1 = *reinterpret_cast<const float4*>(hr + col + 4);
-      const float4 p0 = sum_slices4(part, SK, T, d, t, col);
-      const float4 p1 = sum_slices4(part, SK, T, d, t, col + 4);
-      v[j][0] = h0.x + p0.x; v[j][1] = h0.y + p0.y; v[j][2] = h0.z + p0.z; v[j][3] = h0.w + p0.w;
-      v[j][4] = h1.x + p1.x; v[j][5] = h1.y + p1.y; v[j][6] = h1.z + p1.z; v[j][7] = h1.w + p1.w;
+      for (int e = 0; e < 8; ++e) ss = fmaf(v[j][e], v[j][e], ss);
     }
-    *reinterpret_cast<float4*>(hr + col) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
-    *reinterpret_cast<float4*>(hr + col + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ss = fmaf(v[j][e], v[j][e], ss);
   }
-  ss = block_sum256(ss, sh);
+  ss = block_sum_norm(ss, sh);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
   for (int j = 0; j < MAXCH; ++j) {
-    const int ch = threadIdx.x + 256 * j;
-    if (ch >= nch) break;
-    const int col = ch * 8;
-    float o[8];
+    const int ch = threadIdx.x + NORM_THREADS * j;
+    if (ch < nch) {
+      float o[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = v[j][e] * r * gain[col + e];
-    store8<DT>(xout, t, col, x_S, o);
+      for (int e = 0; e < 8; ++e) o[e] = v[j][e] * r * gn[j][e];
+      store8<DT>(xout, t, ch * 8, x_S, o);
+    }
   }
 }
 
@@ -486,6 +503,7 @@ struct AttnArgs {
   float scale_log2;         // log2(e) / sqrt(hd)
   float* part;              // [splits][Hkv][ncols][hd + 2]
   int max_pages;            // pages per layer in the pool
+  int ptable_len;           // page-table entries (multiple of 4, 16-byte aligned)
 };
 
 constexpr int SPLIT = 256;   // keys per split (4 sub-tiles of 64)
@@ -632,22 +650,51 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   unsigned char* Vall = lds + NSUB * LY::KSUB;
 
   const int gkv = blockIdx.x, sp = blockIdx.y, qgrp = blockIdx.z;
-  if (sp >= a.info[1]) return;          // the grid covers the longest context
+  // (n, splits in use) with one vector load
+  const uint2 inf = bload64<0>(make_rsrc(a.info, 8), 0);
+  const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
+  if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, c = lane & 15;
-  const int n = a.info[0];
   const int nkeys = n + a.T;            // slots written so far
   const int base0 = sp * SPLIT;
   const int nsub = min(NSUB, (nkeys - base0 + 63) / 64);
+
+  // wave -> (query tile of this workgroup, sub-tile of the split); the query
+  // fragments (B operand: column qc, head dims s*KS + grp*EPL ..) are fetched
+  // together with the staging loads
+  const int nqt = (a.ncols + 15) / 16;
+  const int qi = wv / NSUB, st = wv % NSUB;
+  const int qt = qgrp * ATT_QT + qi;
+  const bool work = qt < nqt && st < nsub;     // uniform per wave
+  const int qc = qt * 16 + c;
+  const bool colok = qc < a.ncols;
+  const int t = colok ? qc / a.G : 0;
+  const int head = gkv * a.G + (colok ? qc % a.G : 0);
+  const int mypos = colok ? a.pos[t] : -1;
+  const int base = base0 + st * 64;
+  uint4 qf[NS];
+  {
+    const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.T * a.H * ROWB));
+    const unsigned qb = (unsigned)(((size_t)t * a.H + head) * ROWB);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, (work && colok) ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
+  }
 
   // ---- stage every sub-tile of the split with one batch of loads ----
   {
     const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
     const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
     constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
+    // the split's NSUB page numbers with one vector load (scalar loads of the
+    // uniform addresses would each wait for the previous one)
     int pg[NSUB];
-#pragma unroll
-    for (int st = 0; st < NSUB; ++st) pg[st] = st < nsub ? a.ptable[(base0 >> 6) + st] : 0;
+    {
+      static_assert(NSUB == 4, "one 16-byte load of page numbers");
+      const auto pr = make_rsrc(a.ptable, (unsigned)(a.ptable_len * 4));
+      const uint4 p4 = bload<0>(pr, (unsigned)((base0 >> 6) * 4));
+      pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
+    }
     uint4 tmp[LY::PER];
     unsigned dst[LY::PER];
 #pragma unroll
@@ -703,31 +750,11 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  // wave -> (query tile of this workgroup, sub-tile of the split)
-  const int nqt = (a.ncols + 15) / 16;
-  const int qi = wv / NSUB, st = wv % NSUB;
-  const int qt = qgrp * ATT_QT + qi;
-  const bool work = qt < nqt && st < nsub;     // uniform per wave
-  const int qc = qt * 16 + c;
-  const bool colok = qc < a.ncols;
-  const int t = colok ? qc / a.G : 0;
-  const int head = gkv * a.G + (colok ? qc % a.G : 0);
-  const int mypos = colok ? a.pos[t] : -1;
-  const int base = base0 + st * 64;
-
   float m = -INFINITY, l = 0.f;
   f32x4 o[ND];
 #pragma unroll
   for (int i = 0; i < ND; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (work) {
-    // query fragments (B operand): column qc, head dims [s*KS + grp*EPL, +EPL)
-    uint4 qf[NS];
-    const unsigned char* qb =
-        reinterpret_cast<const unsigned char*>(a.q) + ((size_t)t * a.H + head) * ROWB;
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      qf[s] = colok ? *reinterpret_cast<const uint4*>(qb + (s * KS + grp * EPL) * ESZ)
-                    : make_uint4(0, 0, 0, 0);
     // A tree row at depth j sits at position n + j and sees, at positions
     // n+1 .. n+j, its ancestors in depth order: exactly what the chain along
     // its path would hold there.  Sub-tiles reaching those positions are
@@ -878,40 +905,48 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
 constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 
 // Merge the splits of every (row, head) in split order; write the attention
-// output as packed activations of the O projection.  4 dims per thread.
+// output as packed activations of the O projection.  4 dims per thread.  The
+// state of every split the grid may have written (max_splits, fixed at launch)
+// is fetched in one batch; only the first info[1] take part.
 template <int DT, int HD>
 __global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part,
-                                                              const int* __restrict__ info,
+                                                              const int* __restrict__ info, int max_splits,
                                                               int Hkv, int G, int ncols, int H,
                                                               void* __restrict__ xout, int x_S) {
-  const int nsplit = info[1];
   const int t = blockIdx.x / H, j = blockIdx.x % H;
   const int gkv = j / G, qc = t * G + (j % G);
   const int dim = threadIdx.x * 4;
   float ms[MAX_SPLITS], ls[MAX_SPLITS];
-  float M = -INFINITY;
+  float4 os[MAX_SPLITS];
+  // vector (buffer) loads throughout: the (m, l) addresses are uniform, and
+  // scalar loads of them would be serialised one round trip at a time
+  const auto pr = make_rsrc(part, (unsigned)((size_t)max_splits * Hkv * ncols * (HD + 2) * 4));
 #pragma unroll
   for (int s = 0; s < MAX_SPLITS; ++s) {
-    ms[s] = -INFINITY;
-    ls[s] = 0.f;
-    if (s < nsplit) {
-      const float* p = part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2);
-      ms[s] = p[HD];
-      ls[s] = p[HD + 1];
-      if (ls[s] > 0.f) M = fmaxf(M, ms[s]);
+    if (s < max_splits) {
+      const unsigned off = (unsigned)((((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2) * 4);
+      const uint2 ml = bload64<0>(pr, off + HD * 4);
+      ms[s] = __uint_as_float(ml.x);
+      ls[s] = __uint_as_float(ml.y);
+      const uint4 ov = bload<0>(pr, off + (unsigned)dim * 4);
+      os[s] = make_float4(__uint_as_float(ov.x), __uint_as_float(ov.y), __uint_as_float(ov.z), __uint_as_float(ov.w));
     }
   }
+  const int nsplit = info[1];
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s)
+    if (s < nsplit && ls[s] > 0.f) M = fmaxf(M, ms[s]);
   float L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < MAX_SPLITS; ++s) {
     if (s >= nsplit || !(ls[s] > 0.f)) continue;
     const float w = exp2f(ms[s] - M);
-    const float4 o = *reinterpret_cast<const float4*>(part + (((size_t)s * Hkv + gkv) * ncols + qc) * (HD + 2) + dim);
     L = fmaf(ls[s], w, L);
-    O[0] = fmaf(o.x, w, O[0]);
-    O[1] = fmaf(o.y, w, O[1]);
-    O[2] = fmaf(o.z, w, O[2]);
-    O[3] = fmaf(o.w, w, O[3]);
+    O[0] = fmaf(os[s].x, w, O[0]);
+    O[1] = fmaf(os[s].y, w, O[1]);
+    O[2] = fmaf(os[s].z, w, O[2]);
+    O[3] = fmaf(os[s].w, w, O[3]);
   }
   const size_t fi = frag_index<DT>(t, j * HD + dim, x_S);
   if (DT == DT_BF16) {
@@ -1061,7 +1096,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   auto last = [] { return hipGetLastError(); };
 
   if ((e = timed(prof, PC_NORM, st, [&] {
-         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(T), dim3(256), 0, st, m.embed, w.tok, w.h,
+         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(T), dim3(NORM_THREADS), 0, st, m.embed, w.tok, w.h,
                             w.part, 1, T, m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
          return last();
        })) != hipSuccess)
@@ -1093,6 +1128,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     aa.scale_log2 = 1.4426950408889634f / sqrtf((float)m.hd);
     aa.part = w.attn_part;
     aa.max_pages = m.max_pages;
+    aa.ptable_len = ((m.max_ctx + 63) / 64 + 3) & ~3;
     if ((e = timed(prof, PC_ATTN, st, [&] {
            // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
            const dim3 grid(m.Hkv, nsplit, (nqt + ATT_QT - 1) / ATT_QT);
@@ -1105,7 +1141,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
            hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(T * m.H), dim3(HD / 4), 0, st, w.attn_part,
-                              w.info, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
+                              w.info, w.max_splits, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
       return e;
@@ -1113,7 +1149,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, T, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h, w.part,
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
                               sk_q, T, lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
@@ -1132,7 +1168,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     const float* gn = (l + 1 < m.L) ? m.layers[l + 1].attn_gain : m.final_gain;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(256), 0, st, nullptr, nullptr, w.h, w.part,
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
                               sk_f, T, gn, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
