@@ -139,6 +139,34 @@ def cpu_baseline(shape, weights, k: int, ctx: int, layers: int, emitted_per_step
     }
 
 
+def other_config(ee, name: str, k: int, ctx: int, reps: int = 60) -> dict:
+    """Verify latency of another model shape at a fixed context: drafts are
+    the model's own next k tokens (all accepted); the cache is rolled back to
+    `ctx` after every step."""
+    from workloads import gen_weights, get_shape, zipf_tokens
+    shape = get_shape(name)
+    weights = gen_weights(shape, seed=1234)
+    eng = ee.Engine(shape, weights, max_ctx=ctx + k + 2, k_max=k)
+    prompt = zipf_tokens(shape.vocab, ctx, seed=42)
+    first = eng.prefill(0, prompt)
+    cont = [eng.verify(0, [])[1] for _ in range(k)]
+    lat = []
+    for i in range(reps):
+        eng.rollback(0, ctx, first)
+        ts = time.perf_counter()
+        a, _, _ = eng.verify(0, cont)
+        if i >= 10:
+            lat.append(time.perf_counter() - ts)
+        assert a == k
+    eng.close()
+    p50 = float(np.percentile(lat, 50))
+    tb = step_bytes(shape, k + 1, ctx)["total"]
+    return {"model": f"{name} Llama-style random-init {shape.dtype}", "k": k, "ctx": ctx,
+            "p50_ms": round(p50 * 1e3, 4), "p90_ms": round(float(np.percentile(lat, 90)) * 1e3, 4),
+            "algorithmic_bytes": tb, "hbm_frac": round(tb / p50 / 1e9 / HBM_PEAK_GBS, 4),
+            "tokens_per_s_full_acceptance": round((k + 1) / p50, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,7 +190,7 @@ def main():
     import torch
 
     import paper_2506_02780_amd as ee
-    from workloads import gen_weights, get_shape, inject_edits, zipf_tokens
+    from workloads import gen_weights, get_shape, inject_edits, random_tree, tree_tokens, zipf_tokens
 
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     shape = get_shape(args.config)
@@ -170,8 +198,8 @@ def main():
     t0 = time.perf_counter()
     weights = gen_weights(shape, seed=1234)
     log(f"[bench] weights drawn in {time.perf_counter() - t0:.1f}s")
-    max_ctx = ctx + args.gen + K + 2
-    eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=max(K, 1))
+    max_ctx = ctx + args.gen + 66
+    eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=64)
     if args.eager:
         eng.use_graphs(False)
     log(f"[bench] engine ready at {time.perf_counter() - t0:.1f}s")
@@ -236,17 +264,36 @@ def main():
     gu_alg = gateup_bytes(shape, T)
 
     # verify latency at exactly `ctx` committed positions (rollback after every step)
-    fixed = []
+    def fixed_ctx(draft, parent=None, reps=60):
+        lat, acc = [], []
+        for i in range(reps):
+            eng.rollback(0, ctx, first)
+            ts = time.perf_counter()
+            a, _, _ = eng.verify(0, draft, parent)
+            if i >= 10:
+                lat.append(time.perf_counter() - ts)
+                acc.append(a)
+        return float(np.percentile(lat, 50)), float(np.percentile(lat, 90)), float(np.mean(acc))
+
     d = code[1:1 + K]
-    for i in range(60):
-        eng.rollback(0, ctx, first)
-        ts = time.perf_counter()
-        eng.verify(0, d)
-        if i >= 10:
-            fixed.append(time.perf_counter() - ts)
-    p50 = float(np.percentile(fixed, 50))
-    p90 = float(np.percentile(fixed, 90))
+    p50, p90, _ = fixed_ctx(d)
     sb = step_bytes(shape, T, ctx)
+
+    # K sweep and a 64-node draft tree at the same context; drafts follow the
+    # model's own continuation (G), so every draft token is accepted
+    def lat_entry(kk, lat50, lat90, acc):
+        tb = step_bytes(shape, kk + 1, ctx)["total"]
+        return {"p50_ms": round(lat50 * 1e3, 4), "p90_ms": round(lat90 * 1e3, 4),
+                "hbm_frac": round(tb / lat50 / 1e9 / HBM_PEAK_GBS, 4),
+                "accepted": round(acc, 2), "tokens_per_s_at_this_acceptance": round((acc + 1) / lat50, 1)}
+    k_sweep = {}
+    for kk in (0, 8, 16, 32, 64):
+        l50, l90, acc = fixed_ctx(list(G[1:1 + kk]))
+        k_sweep[str(kk)] = lat_entry(kk, l50, l90, acc)
+    parent = random_tree(64, max_depth=8, max_branch=3, seed=11)
+    ttoks = tree_tokens(parent, G[1:9], shape.vocab, seed=11)
+    l50, l90, acc = fixed_ctx(ttoks, parent)
+    tree64 = dict(lat_entry(64, l50, l90, acc), nodes=64, max_depth=8, max_branch=3)
 
     # a plain device copy of known size, so that hardware byte counters read on
     # this run can be scaled against it
@@ -302,13 +349,17 @@ def main():
             "bytes_per_launch": gu_alg,
         },
         "breakdown_ms_per_step": brk,
+        "k_sweep_at_ctx": k_sweep,
+        "tree64_at_ctx": tree64,
         "lossless_check": "emitted stream equals the GPU's own greedy output",
     }
+    eng.close()
+    if args.config == "7b":
+        result["other_configs"] = {"1b_k16_ctx1024": other_config(ee, "1b", 16, 1024)}
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         result["cpu_baseline"] = cpu_baseline(shape, weights, K, ctx, args.cpu_layers,
                                               emitted / args.steps)
-    eng.close()
     print(json.dumps(result), flush=True)
 
 

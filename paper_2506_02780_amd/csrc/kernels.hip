@@ -516,20 +516,22 @@ __device__ __forceinline__ uint2 bload64(__amdgpu_buffer_rsrc_t r, unsigned off)
   return make_uint2(v.x, v.y);
 }
 
-constexpr int ATT_THREADS = 1024;
-constexpr int ATT_QT = ATT_THREADS / 64 / NSUB;   // query tiles per workgroup
+// workgroup size: 16 waves (4 query tiles x 4 sub-tiles); the tree variant
+// runs 8 waves (2 query tiles) so that its gather loop has 256 registers
+constexpr int att_threads(bool tree) { return tree ? 512 : 1024; }
+constexpr int att_qt(bool tree) { return att_threads(tree) / 64 / NSUB; }
 
 // LDS image of one split: K rows [NSUB][64][HD] and V^T [NSUB][HD][64], rows
 // padded by 16 bytes to spread banks.
-template <int DT, int HD> struct AttnLds {
+template <int DT, int HD, int THREADS> struct AttnLds {
   static constexpr int ESZ = Geo<DT>::ESZ;
   static constexpr int ROWB = HD * ESZ, KROW = ROWB + 16, VROW = 64 * ESZ + 16;
   static constexpr int KSUB = 64 * KROW, VSUB = HD * VROW;
   static constexpr int KV_BYTES = NSUB * (KSUB + VSUB);
-  static constexpr int ST_BYTES = (ATT_THREADS / 64) * (HD * 17 + 32) * 4;   // merge states
+  static constexpr int ST_BYTES = (THREADS / 64) * (HD * 17 + 32) * 4;   // merge states
   static constexpr int BYTES = KV_BYTES > ST_BYTES ? KV_BYTES : ST_BYTES;
   static constexpr int UNITS = 2 * 64 * HD * ESZ / 16;             // uint4 per sub-tile (K + V)
-  static constexpr int PER = (NSUB * UNITS + ATT_THREADS - 1) / ATT_THREADS;
+  static constexpr int PER = (NSUB * UNITS + THREADS - 1) / THREADS;
 };
 
 // One 64-key sub-tile for the wave's 16 query columns: scores S^T = K Q^T
@@ -543,12 +545,13 @@ template <int DT, int HD> struct AttnLds {
 // is <= the column's own.  A column's result depends only on its query, the
 // key/value data and the positions, never on the other columns.  o is
 // accumulated into (the caller clears it); columns with own == false add
-// exact zeros to it.  STREAMV fetches each value fragment right before its
-// MFMAs (fewer live registers; the same arithmetic in the same order).
-template <int DT, int HD, bool STREAMV, class KFn, class VFn>
-__device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, VFn vfn, int base,
-                                              int mypos, float scale_log2, int grp, bool own, float& m,
-                                              float& l, f32x4 (&o)[HD / 16]) {
+// exact zeros to it.  vprep(j) runs before the value fragments of PV step j
+// (k2 or kt) are fetched.  STREAMV fetches each value fragment right before
+// its MFMAs (fewer live registers; the same arithmetic in the same order).
+template <int DT, int HD, bool STREAMV, class KFn, class VFn, class VPrep>
+__device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, VFn vfn, VPrep vprep,
+                                              int base, int mypos, float scale_log2, int grp, bool own,
+                                              float& m, float& l, f32x4 (&o)[HD / 16]) {
   constexpr int NS = HD / Geo<DT>::KS, ND = HD / 16;
   f32x4 sacc[4];
 #pragma unroll
@@ -591,6 +594,7 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
     // bits), so the weights of the value rows keep near-fp32 precision.
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
+      vprep(k2);
       uint32_t ph[8], pl[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -622,6 +626,7 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
   } else {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
+      vprep(kt);
       const uint4 pf = make_uint4(__float_as_uint(sacc[kt][0]), __float_as_uint(sacc[kt][1]),
                                   __float_as_uint(sacc[kt][2]), __float_as_uint(sacc[kt][3]));
 #pragma unroll
@@ -639,8 +644,9 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
 // A column's arithmetic depends only on the key positions, never on T or on
 // which workgroup ran it; keys it cannot see contribute exact zeros.
 template <int DT, int HD, bool TREE>
-__global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
-  using LY = AttnLds<DT, HD>;
+__global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
+  constexpr int ATT_THREADS = att_threads(TREE), ATT_QT = att_qt(TREE);
+  using LY = AttnLds<DT, HD, ATT_THREADS>;
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
   constexpr int NS = HD / KS;          // fragments along head_dim
   constexpr int ND = HD / 16;          // output dim tiles
@@ -677,8 +683,11 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   {
     const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.T * a.H * ROWB));
     const unsigned qb = (unsigned)(((size_t)t * a.H + head) * ROWB);
+    // (tree: waves past the staged sub-tiles may gather, so every wave of a
+    // live query tile needs its queries)
+    const bool need = TREE ? qt < nqt : work;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, (work && colok) ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
+    for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, (need && colok) ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
   }
 
   // ---- stage every sub-tile of the split with one batch of loads ----
@@ -750,99 +759,187 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   }
   __syncthreads();
 
+  // A tree row at depth j sits at position n + j and sees, at positions
+  // n+1 .. n+j, its ancestors in depth order: exactly what the chain along its
+  // path would hold there.  Sub-tiles reaching those positions ("gather"
+  // sub-tiles g0..g1 of the query tile) are computed once per block row, from
+  // keys and values gathered by position; the rows of the tile are dealt out
+  // to its NSUB waves.  Every other sub-tile holds committed keys and the
+  // pending row only, the same for every row, and is read from the staged
+  // image as in the linear case.  The waves of sub-tiles g0 .. NSUB-1 do the
+  // gathering (sub-tiles past g1 lie beyond every row of the tile: their state
+  // is empty), each serving one gather sub-tile and a share of the rows.
+  int g0 = 0, g1 = -1;
+  if (TREE) {
+    int mx = mypos;
+    mx = max(mx, __shfl_xor(mx, 1));
+    mx = max(mx, __shfl_xor(mx, 2));
+    mx = max(mx, __shfl_xor(mx, 4));
+    mx = max(mx, __shfl_xor(mx, 8));   // uniform: the query tile's largest position
+    if (mx > n && mx >= base0) {
+      g0 = n + 1 >= base0 ? (n + 1 - base0) >> 6 : 0;
+      g1 = min(nsub - 1, (mx - base0) >> 6);
+    }
+  }
+  const bool worker = TREE && g1 >= g0 && st >= g0;
+
   float m = -INFINITY, l = 0.f;
   f32x4 o[ND];
 #pragma unroll
   for (int i = 0; i < ND; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (work) {
-    // A tree row at depth j sits at position n + j and sees, at positions
-    // n+1 .. n+j, its ancestors in depth order: exactly what the chain along
-    // its path would hold there.  Sub-tiles reaching those positions are
-    // computed once per block row of the tile, from keys and values gathered
-    // by position; every other sub-tile holds committed keys and the pending
-    // row only, the same for every row, and is read from the staged image.
-    bool gather = false;
-    if (TREE) {
-      int mx = mypos;
-      mx = max(mx, __shfl_xor(mx, 1));
-      mx = max(mx, __shfl_xor(mx, 2));
-      mx = max(mx, __shfl_xor(mx, 4));
-      mx = max(mx, __shfl_xor(mx, 8));
-      gather = mx > n && base + 63 > n && base <= mx;   // uniform: mx is a wave maximum
+  if (work && !worker) {
+    const unsigned char* Ks = Kall + st * LY::KSUB;
+    const unsigned char* Vt = Vall + st * LY::VSUB;
+    auto kfn = [&](int kt, int s) {
+      return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+    };
+    auto vfn = [&](int dt, int j) {
+      const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
+      if (DT == DT_BF16) {
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
+        return make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+      return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
+    };
+    subtile_state<DT, HD, false>(qf, kfn, vfn, [](int) {}, base, mypos, a.scale_log2, grp, true, m, l, o);
+  }
+
+  // a gathering wave serves sub-tile g0 + gi (positions n+1 .. n+64 span at
+  // most two sub-tiles) and its rows t_lo + kk, t_lo + kk + nw, ... (kk-th of
+  // the nw waves serving that sub-tile), accumulating in o
+  const int t_lo = (qt * 16) / a.G, t_hi = (min(qt * 16 + 15, a.ncols - 1)) / a.G;
+  const int ng = g1 - g0 + 1, wk = st - g0;
+  const int gi = worker ? wk % ng : 0, kk = worker ? wk / ng : 0;
+  const int nw = worker ? (NSUB - g0 - gi + ng - 1) / ng : 1;
+  if (worker && qt < nqt && t_lo + kk <= t_hi) {
+    const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
+    const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
+    // Gathered slots never precede the sub-tile: a committed key keeps its
+    // position, and the ancestor shown at position n + j is a block row of
+    // index >= j, i.e. slot >= n + j.  So when the block ends inside the staged
+    // split (the usual case) every gathered slot is staged: gather from LDS;
+    // else from the KV pool.  Uniform over the workgroup.
+    const bool from_lds = nkeys <= base0 + 64 * nsub;
+    // pages of the slots a gather sub-tile can touch, [base0 + 64 g0, n + T):
+    // at most four 64-slot pages, fetched once
+    const int pw0 = (base0 >> 6) + g0;
+    int pgt[4];
+    {
+      const auto pr = make_rsrc(a.ptable, (unsigned)(a.ptable_len * 4));
+      const unsigned o4 = (unsigned)(pw0 * 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pgt[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(pr, o4 + 4 * i, 0, 0);
     }
-    if (!gather) {
-      const unsigned char* Ks = Kall + st * LY::KSUB;
-      const unsigned char* Vt = Vall + st * LY::VSUB;
-      auto kfn = [&](int kt, int s) {
-        return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+    // row tr's path (lane j holds the block row at depth j + 1) and position;
+    // the next row's are fetched while the current one is computed
+    const auto pathr = make_rsrc(a.path, (unsigned)(a.T * 64));
+    const auto posr = make_rsrc(a.pos, (unsigned)(a.T * 4));
+    int tr = t_lo + kk;
+    uint32_t pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)(tr * 64 + lane), 0, 0);
+    int ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)(tr * 4), 0, 0);
+    for (; tr <= t_hi; tr += nw) {
+      const int dep = __builtin_amdgcn_readfirstlane(ptr) - n;
+      const int pth_tr = (int)pth;
+      if (tr + nw <= t_hi) {
+        pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)((tr + nw) * 64 + lane), 0, 0);
+        ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)((tr + nw) * 4), 0, 0);
+      }
+      // physical slot holding position kp on row tr's path (-1: hidden); the
+      // lane shuffle runs on every lane
+      auto slot_of = [&](int kp) {
+        const int j = min(max(kp - n - 1, 0), 63);
+        const int anc = n + (__shfl(pth_tr, j) & 0xff);
+        return kp <= n ? kp : (kp - n <= dep ? anc : -1);
       };
-      auto vfn = [&](int dt, int j) {
-        const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-        if (DT == DT_BF16) {
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
-          return make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
-        return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
+      // every column accumulates; only row tr's columns get non-zero weights
+      const bool own = colok && t == tr;
+      constexpr int NVK = DT == DT_BF16 ? 8 : 4;   // value keys of one PV step per lane
+      // value key i of PV step j: bf16 32j + 16(i/4) + 4grp + i%4, fp32 16j + 4grp + i
+      auto vkey = [&](int j, int i) {
+        return DT == DT_BF16 ? 32 * j + 16 * (i >> 2) + 4 * grp + (i & 3) : 16 * j + 4 * grp + i;
       };
-      subtile_state<DT, HD, false>(qf, kfn, vfn, base, mypos, a.scale_log2, grp, true, m, l, o);
-    } else {
-      const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
-      const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
-      const int t_lo = (qt * 16) / a.G, t_hi = (min(qt * 16 + 15, a.ncols - 1)) / a.G;
-      for (int tr = t_lo; tr <= t_hi; ++tr) {
-        const int dep = a.pos[tr] - n;
-        // physical slot holding position kp on row tr's path (-1: hidden)
-        auto slot_of = [&](int kp) {
-          if (kp <= n) return kp;
-          return kp - n <= dep ? n + (int)a.path[tr * 64 + (kp - n - 1)] : -1;
-        };
-        // byte offset of slot ps's K row (kv = 0) or V^T column (kv = 1)
-        auto off_of = [&](int ps, int kv) {
-          if (ps < 0) return OOB;
-          const int page = a.ptable[ps >> 6];
-          return (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ +
-                            (size_t)(ps & 63) * (kv ? 1 : HD) * ESZ);
-        };
-        unsigned koff[4];
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) koff[kt] = off_of(slot_of(base + 16 * kt + c), 0);
-        constexpr int NVK = 16;                      // value keys held per lane
-        unsigned voff[NVK];
-#pragma unroll
-        for (int i = 0; i < NVK; ++i) {
-          // bf16: key 32(i/8) + 16((i%8)/4) + 4grp + i%4;  fp32: key 16(i/4) + 4grp + i%4
-          const int key = DT == DT_BF16 ? 32 * (i >> 3) + 16 * ((i >> 2) & 1) + 4 * grp + (i & 3)
-                                        : 16 * (i >> 2) + 4 * grp + (i & 3);
-          voff[i] = off_of(slot_of(base + key), 1);
-        }
-        auto kfn = [&](int kt, int s) {
-          return bload<0>(rs, koff[kt] == OOB ? OOB : koff[kt] + (unsigned)((s * KS + grp * EPL) * ESZ));
-        };
-        auto vfn = [&](int dt, int j) {
-          const unsigned drow = (unsigned)((16 * dt + c) * 64 * ESZ);
-          uint32_t w[4];
-          if (DT == DT_BF16) {
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              const int i0 = 8 * j + 2 * h;
-              const uint32_t x0 = __builtin_amdgcn_raw_buffer_load_b16(rs, voff[i0] == OOB ? OOB : voff[i0] + drow, 0, 0);
-              const uint32_t x1 = __builtin_amdgcn_raw_buffer_load_b16(rs, voff[i0 + 1] == OOB ? OOB : voff[i0 + 1] + drow, 0, 0);
-              w[h] = (x0 & 0xffffu) | (x1 << 16);
-            }
-          } else {
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              const int i0 = 4 * j + h;
-              w[h] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff[i0] == OOB ? OOB : voff[i0] + drow, 0, 0);
-            }
-          }
-          return make_uint4(w[0], w[1], w[2], w[3]);
-        };
-        // every column accumulates; only row tr's columns get non-zero weights
-        const bool own = colok && t == tr;
+      {
+        const int gbase = base0 + 64 * (g0 + gi);
         float mt, lt;
-        subtile_state<DT, HD, true>(qf, kfn, vfn, base, mypos, a.scale_log2, grp, own, mt, lt, o);
+        if (from_lds) {
+          // staged row of each key; hidden keys (weight 0) read a staged row
+          auto row_of = [&](int kp) {
+            const int ps = slot_of(kp);
+            return (ps < 0 ? max(n, base0) : ps) - base0;
+          };
+          int krow[4];
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt) krow[kt] = row_of(gbase + 16 * kt + c);
+          auto kfn = [&](int kt, int s) {
+            const int r = krow[kt];
+            return *reinterpret_cast<const uint4*>(Kall + (r >> 6) * LY::KSUB + (r & 63) * KROW +
+                                                   (s * KS + grp * EPL) * ESZ);
+          };
+          int vrow[NVK];
+          auto vprep = [&](int j) {
+#pragma unroll
+            for (int i = 0; i < NVK; ++i) vrow[i] = row_of(gbase + vkey(j, i));
+          };
+          auto vfn = [&](int dt, int j) {
+            const unsigned char* vd = Vall + (16 * dt + c) * VROW;
+            auto elt = [&](int i) -> uint32_t {
+              const int r = vrow[i];
+              const unsigned char* src = vd + (r >> 6) * LY::VSUB + (r & 63) * ESZ;
+              return DT == DT_BF16 ? (uint32_t)*reinterpret_cast<const uint16_t*>(src)
+                                   : *reinterpret_cast<const uint32_t*>(src);
+            };
+            uint32_t w[4];
+            if (DT == DT_BF16) {
+#pragma unroll
+              for (int h = 0; h < 4; ++h) w[h] = elt(2 * h) | (elt(2 * h + 1) << 16);
+            } else {
+#pragma unroll
+              for (int h = 0; h < 4; ++h) w[h] = elt(h);
+            }
+            return make_uint4(w[0], w[1], w[2], w[3]);
+          };
+          subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
+        } else {
+          // byte offset in the KV pool of slot ps's K row (kv = 0) or V^T column (kv = 1)
+          auto off_of = [&](int ps, int kv) {
+            if (ps < 0) return OOB;
+            const int pi = (ps >> 6) - pw0;             // 0..3 (see pw0)
+            const int page = pi == 0 ? pgt[0] : pi == 1 ? pgt[1] : pi == 2 ? pgt[2] : pgt[3];
+            return (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ +
+                              (size_t)(ps & 63) * (kv ? 1 : HD) * ESZ);
+          };
+          unsigned koff[4];
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt) koff[kt] = off_of(slot_of(gbase + 16 * kt + c), 0);
+          auto kfn = [&](int kt, int s) {
+            return bload<0>(rs, koff[kt] == OOB ? OOB : koff[kt] + (unsigned)((s * KS + grp * EPL) * ESZ));
+          };
+          unsigned voff[NVK];
+          auto vprep = [&](int j) {
+#pragma unroll
+            for (int i = 0; i < NVK; ++i) voff[i] = off_of(slot_of(gbase + vkey(j, i)), 1);
+          };
+          auto vfn = [&](int dt, int j) {
+            const unsigned drow = (unsigned)((16 * dt + c) * 64 * ESZ);
+            auto elt = [&](int i) -> uint32_t {
+              const unsigned off = voff[i] == OOB ? OOB : voff[i] + drow;
+              return DT == DT_BF16 ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0)
+                                   : __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+            };
+            uint32_t w[4];
+            if (DT == DT_BF16) {
+#pragma unroll
+              for (int h = 0; h < 4; ++h) w[h] = (elt(2 * h) & 0xffffu) | (elt(2 * h + 1) << 16);
+            } else {
+#pragma unroll
+              for (int h = 0; h < 4; ++h) w[h] = elt(h);
+            }
+            return make_uint4(w[0], w[1], w[2], w[3]);
+          };
+          // all value fragments of a PV step are fetched before its MFMAs
+          subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
+        }
         if (own) {
           m = mt;
           l = lt;
@@ -852,21 +949,34 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_kernel(AttnArgs a) {
   }
 
   // sub-tile states -> LDS (over the staged keys, no longer needed); merge in
-  // sub-tile order: M = max m, w = 2^(m - M), L = sum l w, O = sum o w
+  // sub-tile order: M = max m, w = 2^(m - M), L = sum l w, O = sum o w.  A
+  // gather sub-tile's slot is filled row by row by the waves that computed
+  // the rows.
   __syncthreads();
   float* stO = reinterpret_cast<float*>(lds);                          // [ATT_QT][NSUB][HD][17]
   float* stM = stO + ATT_QT * NSUB * HD * 17;                           // [ATT_QT][NSUB][16]
   float* stL = stM + ATT_QT * NSUB * 16;
-  {
-    float* so = stO + ((size_t)(qi * NSUB + st) * HD) * 17;
+  auto put_state = [&](int slot, const f32x4 (&ov)[ND], float mv, float lv) {
+    float* so = stO + ((size_t)(qi * NSUB + slot) * HD) * 17;
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = o[dt][r];
+      for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = ov[dt][r];
     if (grp == 0) {
-      stM[(qi * NSUB + st) * 16 + c] = m;
-      stL[(qi * NSUB + st) * 16 + c] = l;
+      stM[(qi * NSUB + slot) * 16 + c] = mv;
+      stL[(qi * NSUB + slot) * 16 + c] = lv;
     }
+  };
+  if (!worker) {
+    put_state(st, o, m, l);
+  } else {
+    if (st > g1) {
+      f32x4 z[ND];
+#pragma unroll
+      for (int i = 0; i < ND; ++i) z[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      put_state(st, z, -INFINITY, 0.f);
+    }
+    if (qt < nqt && colok && t >= t_lo + kk && (t - t_lo - kk) % nw == 0) put_state(g0 + gi, o, m, l);
   }
   __syncthreads();
   // thread -> (query tile, column, HD/16 dims)
@@ -1131,11 +1241,12 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     aa.ptable_len = ((m.max_ctx + 63) / 64 + 3) & ~3;
     if ((e = timed(prof, PC_ATTN, st, [&] {
            // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
-           const dim3 grid(m.Hkv, nsplit, (nqt + ATT_QT - 1) / ATT_QT);
+           const int qt = att_qt(aa.tree);
+           const dim3 grid(m.Hkv, nsplit, (nqt + qt - 1) / qt);
            if (aa.tree)
-             hipLaunchKernelGGL((attn_kernel<DT, HD, true>), grid, dim3(ATT_THREADS), 0, st, aa);
+             hipLaunchKernelGGL((attn_kernel<DT, HD, true>), grid, dim3(att_threads(true)), 0, st, aa);
            else
-             hipLaunchKernelGGL((attn_kernel<DT, HD, false>), grid, dim3(ATT_THREADS), 0, st, aa);
+             hipLaunchKernelGGL((attn_kernel<DT, HD, false>), grid, dim3(att_threads(false)), 0, st, aa);
            return last();
          })) != hipSuccess)
       return e;
