@@ -127,6 +127,21 @@ int32_t ee_verify(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t
                   const int32_t* parent, int32_t* accept_len, int32_t* next_token,
                   int32_t* accepted_nodes);
 
+/* ee_verify for n_seq distinct sequences in one block (n_seq <= max_seqs),
+ * all with the same draft length K: drafts[b*K .. b*K + K-1] is the draft of
+ * sequence seqs[b]; parents (NULL: every draft is a linear chain) holds
+ * n_seq arrays of K parent indices laid out the same way; accept_lens[b],
+ * next_tokens[b] and (optional) accepted_nodes[b*K ..] are the results of
+ * sequence seqs[b], exactly as ee_verify defines them.  Each sequence reads
+ * only its own cache, and its rows' arithmetic is the same as in a block of
+ * its own: every result equals that of ee_verify on the sequence alone.
+ * Either every sequence advances or, on error, none does.  Errors: as
+ * ee_verify, plus EE_EINVAL for n_seq outside [1, max_seqs] or a sequence
+ * listed twice. */
+int32_t ee_verify_batch(ee_ctx* ctx, int32_t n_seq, const int32_t* seqs, const int32_t* drafts,
+                        int32_t K, const int32_t* parents, int32_t* accept_lens,
+                        int32_t* next_tokens, int32_t* accepted_nodes);
+
 /* Truncate sequence `seq` to its first new_len committed positions
  * (new_len <= len), release pages wholly beyond them and make pending_token
  * pending.  new_len == 0 with pending_token == -1 empties the sequence (it

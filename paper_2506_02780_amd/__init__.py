@@ -59,6 +59,7 @@ ee_create = _sig("ee_create", _i32, [ctypes.POINTER(EEModelConfig), ctypes.POINT
 ee_destroy = _sig("ee_destroy", _i32, [_vp])
 ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
+ee_verify_batch = _sig("ee_verify_batch", _i32, [_vp, _i32, _pi32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_kv_rollback = _sig("ee_kv_rollback", _i32, [_vp, _i32, _i32, _i32])
 ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
 ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32, _i32, _i32, _pi32, _pi32])
@@ -190,6 +191,34 @@ class Engine:
         _check(ee_verify(self.ctx, seq, dp, k, None, ctypes.byref(a), ctypes.byref(nxt), None), self.ctx)
         self._last_rows = k + 1
         return a.value, nxt.value, None
+
+    def verify_batch(self, seqs, drafts, parents=None):
+        """One block for several sequences; drafts (and parents) are equal-length
+        lists, one per sequence.  Returns [(accept_len, next_token,
+        accepted_nodes or None)] in the order of ``seqs``."""
+        n = len(seqs)
+        k = len(drafts[0]) if n else 0
+        if len(drafts) != n or any(len(d) != k for d in drafts):
+            raise EEError(EE_EINVAL, "one draft per sequence, all of the same length")
+        sq, sp = _i32arr(seqs)
+        d, dp = _i32arr(np.concatenate([np.asarray(x, dtype=np.int32).reshape(-1) for x in drafts])
+                        if n else np.zeros(0, np.int32))
+        acc = np.zeros(max(n, 1), dtype=np.int32)
+        nxt = np.zeros(max(n, 1), dtype=np.int32)
+        nodes = np.zeros(max(n * k, 1), dtype=np.int32)
+        pp = None
+        if parents is not None:
+            if len(parents) != n or any(len(p) != k for p in parents):
+                raise EEError(EE_EINVAL, "parents must match the drafts")
+            p, pp = _i32arr(np.concatenate([np.asarray(x, dtype=np.int32).reshape(-1) for x in parents]))
+        _check(ee_verify_batch(self.ctx, n, sp, dp, k, pp, acc.ctypes.data_as(_pi32), nxt.ctypes.data_as(_pi32),
+                               nodes.ctypes.data_as(_pi32) if parents is not None else None), self.ctx)
+        self._last_rows = n * (k + 1)
+        out = []
+        for b in range(n):
+            a = int(acc[b])
+            out.append((a, int(nxt[b]), nodes[b * k:b * k + a].copy() if parents is not None else None))
+        return out
 
     def rollback(self, seq: int, new_len: int, pending: int):
         _check(ee_kv_rollback(self.ctx, seq, new_len, pending), self.ctx)

@@ -36,14 +36,14 @@ struct Seq {
 
 // Byte offsets of every buffer inside the three caller allocations.
 struct Layout {
-  int Tmax, MT, G, max_splits, pages_per_seq, n_pages;
+  int Tmax, Rmax, MT, G, max_splits, pages_per_seq, ptable_len, n_pages;
   // packed arena
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
   size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
-  size_t s_tok, s_pos, s_prow, s_path, s_ptable, s_info, stage_bytes;
+  size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, stage_bytes;
   size_t kv_layer, kv_total;
 };
 
@@ -85,10 +85,12 @@ Layout make_layout(const ee_model_config* c) {
   const size_t d = c->d_model, hd = c->head_dim, H = c->n_heads, Hkv = c->n_kv_heads;
   const size_t F = c->ffn, V = c->vocab;
   L.Tmax = c->k_max + 1;
-  L.MT = (L.Tmax + 15) / 16;
+  L.Rmax = L.Tmax * c->max_seqs;   // a block holds up to max_seqs sequences
+  L.MT = (L.Rmax + 15) / 16;
   L.G = c->n_heads / c->n_kv_heads;
   L.max_splits = (c->max_ctx + SPLIT - 1) / SPLIT + 1;
   L.pages_per_seq = (c->max_ctx + PAGE - 1) / PAGE;
+  L.ptable_len = (L.pages_per_seq + 3) & ~3;   // 16-byte loads of page numbers
   L.n_pages = L.pages_per_seq * c->max_seqs;
   // packed arena
   size_t o = 0;
@@ -110,13 +112,13 @@ Layout make_layout(const ee_model_config* c) {
   const size_t Tpad = (size_t)L.MT * 16;
   const size_t xcols = std::max(d, H * hd);
   o = 0;
-  L.h = o; o += up(L.Tmax * d * 4);
+  L.h = o; o += up(L.Rmax * d * 4);
   L.xbuf = o; o += up(Tpad * xcols * esz);
   L.zbuf = o; o += up(Tpad * F * esz);
-  L.q = o; o += up(L.Tmax * H * hd * esz);
-  L.part = o; o += up((size_t)L.max_splits * Hkv * L.Tmax * L.G * (hd + 2) * 4);
+  L.q = o; o += up(L.Rmax * H * hd * esz);
+  L.part = o; o += up((size_t)L.max_splits * Hkv * L.Rmax * L.G * (hd + 2) * 4);
   {
-    // split-K partials of the largest GEMM: [slices][Tmax][N]
+    // split-K partials of the largest GEMM: [slices][Rmax][N]
     const int dt = c->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
     const size_t qkvN = (H + 2 * Hkv) * hd;
     size_t mx = 0;
@@ -125,21 +127,22 @@ Layout make_layout(const ee_model_config* c) {
     mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * 2 * F);
     mx = std::max(mx, (size_t)ee::gemm_slices_for((int)F, dt) * d);
     mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * V);
-    L.gpart = o; o += up(mx * L.Tmax * 4);
+    L.gpart = o; o += up(mx * L.Rmax * 4);
   }
-  L.logits = o; o += up(L.Tmax * V * 4);
-  L.amax = o; o += up(L.Tmax * ((V + 2047) / 2048) * 8);
-  L.greedy = o; o += up(L.Tmax * 4);
-  L.result = o; o += up((2 + 64) * 4);
+  L.logits = o; o += up(L.Rmax * V * 4);
+  L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8);
+  L.greedy = o; o += up(L.Rmax * 4);
+  L.result = o; o += up((size_t)c->max_seqs * (2 + 64) * 4);
   // staging block: one host->device copy per call
   size_t so = 0;
-  L.s_tok = so; so += L.Tmax * 4;
-  L.s_pos = so; so += L.Tmax * 4;
-  L.s_prow = so; so += L.Tmax * 4;
-  L.s_path = so; so += L.Tmax * 64;
+  L.s_tok = so; so += L.Rmax * 4;
+  L.s_pos = so; so += L.Rmax * 4;
+  L.s_prow = so; so += L.Rmax * 4;
+  L.s_slot = so; so += L.Rmax * 4;
+  L.s_path = so; so += L.Rmax * 64;
   so = (so + 15) & ~(size_t)15;   // 16-byte loads of page numbers
-  L.s_ptable = so; so += ((L.pages_per_seq + 3) & ~3) * 4;
-  L.s_info = so; so += 4 * 4;
+  L.s_ptable = so; so += (size_t)c->max_seqs * L.ptable_len * 4;
+  L.s_info = so; so += (size_t)c->max_seqs * 4 * 4;
   L.stage_bytes = up(so);
   L.stage = o; o += L.stage_bytes;
   L.rope = o; o += up((size_t)c->max_ctx * (hd / 2) * 8);
@@ -163,7 +166,7 @@ struct ee_ctx {
     hipGraphExec_t exec;
     int prof_pairs;                  // event pairs recorded by the graph's own nodes
   };
-  std::map<std::tuple<int, int, uint32_t>, Captured> graphs;   // (T, mode, profiling mask)
+  std::map<std::tuple<int, int, int, uint32_t>, Captured> graphs;   // (T, B, mode, profiling mask)
   bool graphs_ok = true;             // capture works on this stream
   bool graphs_on = true;             // ee_use_graphs
   unsigned char* packed = nullptr;
@@ -222,8 +225,10 @@ void bind_work(ee_ctx* c) {
   w.tok = reinterpret_cast<int*>(sb + L.s_tok);
   w.pos = reinterpret_cast<int*>(sb + L.s_pos);
   w.prow = reinterpret_cast<int*>(sb + L.s_prow);
+  w.slot = reinterpret_cast<int*>(sb + L.s_slot);
   w.ptable = reinterpret_cast<int*>(sb + L.s_ptable);
   w.info = reinterpret_cast<int*>(sb + L.s_info);
+  w.ptable_len = L.ptable_len;
   w.max_splits = L.max_splits;
 }
 
@@ -270,7 +275,7 @@ hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
 // capture is unavailable (the block then runs eagerly).
 const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
   if (!c->graphs_ok || !c->graphs_on) return nullptr;
-  const auto key = std::make_tuple(step.T, step.mode, prof ? prof->mask : 0u);
+  const auto key = std::make_tuple(step.T, step.B, step.mode, prof ? prof->mask : 0u);
   auto it = c->graphs.find(key);
   if (it != c->graphs.end()) return &it->second;
   hipGraph_t g = nullptr;
@@ -295,19 +300,29 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
   return &slot;
 }
 
-// Stage rows, run the forward + acceptance (+ tree compaction), fetch the
-// result.  Returns EE_OK and fills h_result.
-int run_block(ee_ctx* c, Seq& s, int T, int mode) {
+// Stage the per-sequence state (page tables, committed lengths, the KV slot
+// of every row), run the forward + acceptance (+ tree compaction) of B
+// sequences of T rows whose tokens, positions and parents the caller staged,
+// and fetch the results (record b at h_result + b * (2 + 64)).
+int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode) {
   const Layout& L = c->lay;
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
-  for (size_t i = 0; i < s.pages.size(); ++i) ptab[i] = s.pages[i];
   int* info = reinterpret_cast<int*>(c->h_stage + L.s_info);
-  info[0] = s.len;
-  info[1] = (s.len + T + SPLIT - 1) / SPLIT;
+  int* slot = reinterpret_cast<int*>(c->h_stage + L.s_slot);
+  for (int b = 0; b < B; ++b) {
+    const Seq& s = *seqs[b];
+    for (size_t i = 0; i < s.pages.size(); ++i) ptab[b * L.ptable_len + i] = s.pages[i];
+    info[4 * b + 0] = s.len;
+    info[4 * b + 1] = (s.len + T + SPLIT - 1) / SPLIT;
+    for (int t = 0; t < T; ++t) {
+      const int p = s.len + t;   // block row t lands in slot len + t
+      slot[b * T + t] = s.pages[p / PAGE] * PAGE + p % PAGE;
+    }
+  }
   HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
   HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
   HIP_TRY(c, hipMemcpyAsync(c->ws + L.stage, c->h_stage, L.stage_bytes, hipMemcpyHostToDevice, c->st));
-  const ee::Step step{T, mode};
+  const ee::Step step{T, B, mode};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
   const ee_ctx::Captured* cg = prof ? nullptr : block_graph(c, step, nullptr);
@@ -318,7 +333,8 @@ int run_block(ee_ctx* c, Seq& s, int T, int mode) {
     c->prof.used = 0;
     HIP_TRY(c, launch_block(c, step, prof));
   }
-  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (2 + 64) * sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (size_t)B * (2 + 64) * sizeof(int),
+                            hipMemcpyDeviceToHost, c->st));
   HIP_TRY(c, hipStreamSynchronize(c->st));
   for (int i = 0; prof && i < c->prof.used; ++i) {
     float ms = 0.f;
@@ -326,8 +342,50 @@ int run_block(ee_ctx* c, Seq& s, int T, int mode) {
     c->prof_ms[c->ev_cls[i]] += ms;
     c->prof_n[c->ev_cls[i]] += 1;
   }
-  c->last_T = T;
+  c->last_T = B * T;
   return EE_OK;
+}
+
+// Check the draft of one sequence (K tokens, optional parents) before
+// anything is staged; fills depth[0..K] for trees.
+int check_draft(ee_ctx* c, const int32_t* draft, int K, const int32_t* parent, int* depth) {
+  if (K > 0 && !draft) return fail(c, EE_EINVAL, "draft_tokens is NULL");
+  for (int i = 0; i < K; ++i)
+    if (draft[i] < 0 || draft[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "draft token outside [0, vocab)");
+  if (parent) {
+    depth[0] = 0;
+    for (int i = 0; i < K; ++i) {
+      if (parent[i] < -1 || parent[i] >= i) return fail(c, EE_EINVAL, "parent[i] must be in [-1, i)");
+      depth[i + 1] = depth[parent[i] + 1] + 1;
+    }
+  }
+  return EE_OK;
+}
+
+// Stage rows b*T .. b*T + T - 1: the pending token and the draft, their
+// positions, parent rows and (trees) paths.
+void stage_draft(ee_ctx* c, int b, int T, const Seq& s, const int32_t* draft, const int32_t* parent,
+                 const int* depth) {
+  const Layout& L = c->lay;
+  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok) + b * T;
+  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos) + b * T;
+  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow) + b * T;
+  unsigned char* path = c->h_stage + L.s_path + (size_t)b * T * 64;
+  tok[0] = s.pending;
+  pos[0] = s.len;
+  prow[0] = -1;
+  for (int r = 1; r < T; ++r) {
+    tok[r] = draft[r - 1];
+    if (parent) {
+      prow[r] = parent[r - 1] + 1;
+      pos[r] = s.len + depth[r];
+      // the rows on r's path, by depth (attention sees them at n+1 .. n+depth)
+      for (int x = r, j = depth[r]; x >= 1; x = prow[x], --j) path[r * 64 + j - 1] = (unsigned char)x;
+    } else {
+      prow[r] = r - 1;
+      pos[r] = s.len + r;
+    }
+  }
 }
 
 }  // namespace
@@ -390,7 +448,8 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   };
   hipError_t e;
   if ((e = hipHostMalloc(reinterpret_cast<void**>(&c->h_stage), L.stage_bytes, hipHostMallocDefault)) != hipSuccess ||
-      (e = hipHostMalloc(reinterpret_cast<void**>(&c->h_result), (2 + 64) * sizeof(int), hipHostMallocDefault)) != hipSuccess) {
+      (e = hipHostMalloc(reinterpret_cast<void**>(&c->h_result), (size_t)cfg->max_seqs * (2 + 64) * sizeof(int),
+                          hipHostMallocDefault)) != hipSuccess) {
     hip_fail(c, e, "hipHostMalloc");
     return cleanup(EE_EHIP);
   }
@@ -502,7 +561,8 @@ int32_t ee_prefill(ee_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, int
       pos[r] = s.len + r;
       prow[r] = r - 1;
     }
-    rc = run_block(c, s, T, 0);
+    Seq* one = &s;
+    rc = run_block(c, &one, 1, T, 0);
     if (rc) {   // leave the sequence empty, as before the call
       s.len = len0;
       unreserve(c, s, added);
@@ -525,42 +585,15 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   Seq& s = c->seqs[seq];
   if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
   if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
-  if (K > 0 && !draft) return fail(c, EE_EINVAL, "draft_tokens is NULL");
-  for (int i = 0; i < K; ++i)
-    if (draft[i] < 0 || draft[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "draft token outside [0, vocab)");
-  const Layout& L = c->lay;
-  const int T = K + 1;
-  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
-  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
-  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
-  unsigned char* path = c->h_stage + L.s_path;
   int depth[65];
-  if (parent) {
-    depth[0] = 0;
-    for (int i = 0; i < K; ++i) {
-      if (parent[i] < -1 || parent[i] >= i) return fail(c, EE_EINVAL, "parent[i] must be in [-1, i)");
-      depth[i + 1] = depth[parent[i] + 1] + 1;
-    }
-  }
+  if ((rc = check_draft(c, draft, K, parent, depth))) return rc;
+  const int T = K + 1;
   if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
   int added;
   if (!reserve_pages(c, s, s.len + T, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
-  tok[0] = s.pending;
-  pos[0] = s.len;
-  prow[0] = -1;
-  for (int r = 1; r < T; ++r) {
-    tok[r] = draft[r - 1];
-    if (parent) {
-      prow[r] = parent[r - 1] + 1;
-      pos[r] = s.len + depth[r];
-      // the rows on r's path, by depth (attention sees them at n+1 .. n+depth)
-      for (int x = r, j = depth[r]; x >= 1; x = prow[x], --j) path[r * 64 + j - 1] = (unsigned char)x;
-    } else {
-      prow[r] = r - 1;
-      pos[r] = s.len + r;
-    }
-  }
-  rc = run_block(c, s, T, parent ? 2 : 1);
+  stage_draft(c, 0, T, s, draft, parent, depth);
+  Seq* one = &s;
+  rc = run_block(c, &one, 1, T, parent ? 2 : 1);
   if (rc) {
     unreserve(c, s, added);
     return rc;
@@ -572,6 +605,58 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   *next_token = s.pending;
   if (accepted_nodes)
     for (int i = 0; i < a; ++i) accepted_nodes[i] = c->h_result[2 + i] - 1;
+  return EE_OK;
+}
+
+int32_t ee_verify_batch(ee_ctx* c, int32_t n_seq, const int32_t* seqs, const int32_t* drafts, int32_t K,
+                        const int32_t* parents, int32_t* accept_lens, int32_t* next_tokens,
+                        int32_t* accepted_nodes) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (n_seq < 1 || n_seq > c->cfg.max_seqs) return fail(c, EE_EINVAL, "n_seq outside [1, max_seqs]");
+  if (!seqs || !accept_lens || !next_tokens)
+    return fail(c, EE_EINVAL, "seqs, accept_lens and next_tokens must be non-NULL");
+  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
+  const int T = K + 1;
+  std::vector<int> depth((size_t)n_seq * 65);
+  std::vector<Seq*> ss(n_seq);
+  for (int b = 0; b < n_seq; ++b) {
+    int rc = check_seq(c, seqs[b]);
+    if (rc) return rc;
+    for (int b2 = 0; b2 < b; ++b2)
+      if (seqs[b2] == seqs[b]) return fail(c, EE_EINVAL, "a sequence appears twice in the batch");
+    Seq& s = c->seqs[seqs[b]];
+    if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
+    if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
+    if ((rc = check_draft(c, drafts ? drafts + (size_t)b * K : nullptr, K,
+                          parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65])))
+      return rc;
+    ss[b] = &s;
+  }
+  std::vector<int> added(n_seq, 0);
+  for (int b = 0; b < n_seq; ++b) {
+    if (!reserve_pages(c, *ss[b], ss[b]->len + T, &added[b])) {
+      for (int b2 = 0; b2 <= b; ++b2) unreserve(c, *ss[b2], added[b2]);
+      return fail(c, EE_ECAPACITY, "KV pool exhausted");
+    }
+  }
+  for (int b = 0; b < n_seq; ++b)
+    stage_draft(c, b, T, *ss[b], drafts ? drafts + (size_t)b * K : nullptr,
+                parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65]);
+  const int rc = run_block(c, ss.data(), n_seq, T, parents ? 2 : 1);
+  if (rc) {
+    for (int b = 0; b < n_seq; ++b) unreserve(c, *ss[b], added[b]);
+    return rc;
+  }
+  for (int b = 0; b < n_seq; ++b) {
+    const int* res = c->h_result + (size_t)b * (2 + 64);
+    const int a = res[0];
+    ss[b]->len += 1 + a;
+    ss[b]->pending = res[1];
+    accept_lens[b] = a;
+    next_tokens[b] = res[1];
+    if (accepted_nodes)
+      for (int i = 0; i < a; ++i) accepted_nodes[(size_t)b * K + i] = res[2 + i] - 1;
+  }
   return EE_OK;
 }
 

@@ -56,26 +56,30 @@ struct Model {
   const float2* rope;       // [max_ctx][hd / 2] (cos, sin)
 };
 
-// Per-step device buffers (all inside the caller's workspace).
+// Per-step device buffers (all inside the caller's workspace).  A block holds
+// B sequences of T rows each, R = B * T rows in all (row b*T + t is row t of
+// sequence b); Rmax = max_seqs * (k_max + 1).
 struct Work {
-  float* h;                 // [Tmax, d] residual stream
+  float* h;                 // [Rmax, d] residual stream
   uint4* xbuf;              // packed activations, max(d, H*hd) columns
   uint4* zbuf;              // packed activations, F columns
-  void* q;                  // [Tmax, H, hd] model dtype
-  float* attn_part;         // [splits][Hkv][Tmax*G][hd + 2]
-  float* part;              // GEMM slice partials [SK][T][N]
-  float* logits;            // [Tmax, V]
-  unsigned long long* amax; // [Tmax, ceil(V/2048)]
-  int* greedy;              // [Tmax]
-  int* result;              // [2 + 64]: accept_len, next, accepted rows
+  void* q;                  // [Rmax, H, hd] model dtype
+  float* attn_part;         // [splits][Hkv][Rmax*G][hd + 2]
+  float* part;              // GEMM slice partials [SK][R][N]
+  float* logits;            // [Rmax, V]
+  unsigned long long* amax; // [Rmax, ceil(V/2048)]
+  int* greedy;              // [Rmax]
+  int* result;              // [max_seqs][2 + 64]: accept_len, next, accepted rows
   // staged per call (host -> device)
-  int* tok;                 // [Tmax]
-  int* pos;                 // [Tmax] rotary position of each row
-  int* prow;                // [Tmax] parent row (tree) or r-1
-  unsigned char* path;      // [Tmax][64] tree mode: entry j-1 of row t = block row at
+  int* tok;                 // [Rmax]
+  int* pos;                 // [Rmax] rotary position of each row
+  int* prow;                // [Rmax] parent row within the sequence (tree) or t-1
+  int* slot;                // [Rmax] KV-pool slot (page * 64 + offset) the row's K/V go to
+  unsigned char* path;      // [Rmax][64] tree mode: entry j-1 of row t = block row at
                             // depth j on t's path (row 0, the pending token, is depth 0)
-  int* ptable;              // [max_pages] page of each 64-position block
-  int* info;                // [0] committed positions n, [1] attention splits in use
+  int* ptable;              // [max_seqs][ptable_len] page of each 64-position block
+  int* info;                // [max_seqs][4]: committed positions n, attention splits in use
+  int ptable_len;           // entries per sequence (multiple of 4)
   int max_splits;           // attention splits of the longest context
 };
 
@@ -91,11 +95,12 @@ struct Prof {
 };
 
 // Launch shape of one block.  Everything that changes from step to step
-// (committed length, split count, tokens, positions, pages) is read by the
-// kernels from the staging block, so a captured graph of a (T, mode) shape
-// can be replayed for any step.
+// (committed lengths, split counts, tokens, positions, pages) is read by the
+// kernels from the staging block, so a captured graph of a (T, B, mode)
+// shape can be replayed for any step.
 struct Step {
-  int T;        // rows in the block
+  int T;        // rows per sequence
+  int B;        // sequences in the block
   int mode;     // 0 prefill, 1 linear verify, 2 tree verify
 };
 

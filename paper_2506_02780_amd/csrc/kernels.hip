@@ -171,9 +171,10 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned off) {
 
 struct GemmArgs {
   const uint4* w;       // packed weights [n_tiles][S][64]
-  const uint4* x;       // packed activations [MT][S][64]
-  float* part;          // [SK][T][N]
+  const uint4* x;       // packed activations of this launch's rows [MT][S][64]
+  float* part;          // [SK][Ttot][N]; this launch writes rows row0 .. row0 + T - 1
   int S, SK, SS, T, N, n_tiles;
+  int row0, Ttot;
 };
 
 inline int gemm_slices(int S) {
@@ -232,18 +233,23 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
       for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][m][ln];
       const int t = m * 16 + (ln & 15);
       if (t < a.T) {
-        float* o = a.part + ((size_t)k * a.T + t) * a.N + tile * 16 + 4 * (ln >> 4);
+        float* o = a.part + ((size_t)k * a.Ttot + a.row0 + t) * a.N + tile * 16 + 4 * (ln >> 4);
         *reinterpret_cast<float4*>(o) = make_float4(v.x, v.y, v.z, v.w);
       }
     }
   }
 }
 
+constexpr int GEMM_MAX_ROWS = 80;   // rows one launch holds in registers (MT <= 5)
+
+// Y = X W^T for R rows: launches of at most GEMM_MAX_ROWS rows each (every
+// launch streams the weights once; a row's arithmetic is the same in any
+// launch).
 template <int DT>
-static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int T, float* part,
+static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int R, float* part,
                        hipStream_t st) {
   GemmArgs a;
-  a.w = w; a.x = x; a.part = part; a.T = T; a.N = N;
+  a.w = w; a.part = part; a.N = N; a.Ttot = R;
   a.S = K / Geo<DT>::KS;
   a.SK = gemm_slices(a.S);
   a.SS = (a.S + a.SK - 1) / a.SK;
@@ -252,15 +258,22 @@ static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int T, floa
   if (groups < 1) groups = 1;
   if (groups > a.n_tiles) groups = a.n_tiles;
   const dim3 grid(groups * a.SK), block(GEMM_WAVES * 64);
-  switch ((T + 15) / 16) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2>), grid, block, 0, st, a); break;
-    case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3>), grid, block, 0, st, a); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4>), grid, block, 0, st, a); break;
-    case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5>), grid, block, 0, st, a); break;
-    default: return hipErrorInvalidValue;
+  for (int r0 = 0; r0 < R; r0 += GEMM_MAX_ROWS) {
+    a.row0 = r0;
+    a.T = R - r0 < GEMM_MAX_ROWS ? R - r0 : GEMM_MAX_ROWS;
+    a.x = x + (size_t)(r0 / 16) * a.S * 64;   // r0 is a multiple of 16
+    switch ((a.T + 15) / 16) {
+      case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1>), grid, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2>), grid, block, 0, st, a); break;
+      case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3>), grid, block, 0, st, a); break;
+      case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4>), grid, block, 0, st, a); break;
+      case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5>), grid, block, 0, st, a); break;
+      default: return hipErrorInvalidValue;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 constexpr int MAX_SLICES = 16;   // gemm_slices() never exceeds this for K <= 32768
@@ -383,14 +396,14 @@ __global__ __launch_bounds__(NORM_THREADS) void norm_kernel(const void* __restri
 
 // q/k/v of row t from the QKV partials: rotary on q and k (pairs (i, i+hd/2)
 // at the row's position), q to the block buffer, k and v into the row's KV
-// cache slot n + t (V stored transposed per page).  One thread per pair.
+// pool slot (page * 64 + offset; V stored transposed per page).  One thread
+// per pair.
 template <int DT>
 __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict__ part, int SK, int T,
                                                          int N, int H, int Hkv, int hd,
                                                          const int* __restrict__ pos,
                                                          const float2* __restrict__ rope,
-                                                         const int* __restrict__ ptable,
-                                                         const int* __restrict__ info,
+                                                         const int* __restrict__ rowslot,
                                                          void* __restrict__ q, void* __restrict__ kv_layer) {
   const int t = blockIdx.y;
   const int half = hd >> 1;
@@ -410,8 +423,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
 #pragma unroll
   for (int k = 1; k < MAX_SLICES; ++k)
     if (k < SK) { x1 += p1[k]; x2 += p2[k]; }
-  const int slot = info[0] + t;   // block row t lands in slot n + t
-  const int page = ptable[slot >> 6], sp = slot & 63;
+  const int slot = rowslot[t];
+  const int page = slot >> 6, sp = slot & 63;
   if (head < H + Hkv) {
     const float2 cs = rope[(size_t)pos[t] * half + i];
     const float y1 = x1 * cs.x - x2 * cs.y;
@@ -494,14 +507,15 @@ __global__ __launch_bounds__(256) void logits_kernel(const float* __restrict__ p
 struct AttnArgs {
   const void* q;            // [T][H][hd]
   const void* kv_layer;     // [pages][2][Hkv][64*hd]
-  const int* ptable;
+  const int* ptable;        // [B][ptable_len]
   const int* pos;
-  const unsigned char* path;  // tree: [T][64], entry j-1 = block row at depth j on row t's path
-  const int* info;          // [0] committed positions n, [1] splits in use
-  int T, H, Hkv, G, ncols;
+  const unsigned char* path;  // tree: [B*T][64], entry j-1 = block row at depth j on row t's path
+  const int* info;          // [B][4]: committed positions n, splits in use
+  int T, H, Hkv, G, ncols;  // T rows and ncols = T * G query columns per sequence
+  int B;                    // sequences: rows b*T .. b*T + T - 1, columns b*ncols ..
   int tree;
   float scale_log2;         // log2(e) / sqrt(hd)
-  float* part;              // [splits][Hkv][ncols][hd + 2]
+  float* part;              // [splits][Hkv][B * ncols][hd + 2]
   int max_pages;            // pages per layer in the pool
   int ptable_len;           // page-table entries (multiple of 4, 16-byte aligned)
 };
@@ -655,9 +669,16 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   unsigned char* Kall = lds;
   unsigned char* Vall = lds + NSUB * LY::KSUB;
 
-  const int gkv = blockIdx.x, sp = blockIdx.y, qgrp = blockIdx.z;
+  const int nqt = (a.ncols + 15) / 16;
+  const int qgs = (nqt + ATT_QT - 1) / ATT_QT;   // query-tile groups per sequence
+  const int gkv = blockIdx.x, sp = blockIdx.y, b = blockIdx.z / qgs, qgrp = blockIdx.z % qgs;
+  // this sequence's rows, positions, paths, pages and step state
+  const int rb = b * a.T;
+  const int* pos = a.pos + rb;
+  const unsigned char* path = a.path + (size_t)rb * 64;
+  const int* ptable = a.ptable + b * a.ptable_len;
   // (n, splits in use) with one vector load
-  const uint2 inf = bload64<0>(make_rsrc(a.info, 8), 0);
+  const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
   const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
   if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -669,7 +690,6 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   // wave -> (query tile of this workgroup, sub-tile of the split); the query
   // fragments (B operand: column qc, head dims s*KS + grp*EPL ..) are fetched
   // together with the staging loads
-  const int nqt = (a.ncols + 15) / 16;
   const int qi = wv / NSUB, st = wv % NSUB;
   const int qt = qgrp * ATT_QT + qi;
   const bool work = qt < nqt && st < nsub;     // uniform per wave
@@ -677,12 +697,12 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   const bool colok = qc < a.ncols;
   const int t = colok ? qc / a.G : 0;
   const int head = gkv * a.G + (colok ? qc % a.G : 0);
-  const int mypos = colok ? a.pos[t] : -1;
+  const int mypos = colok ? pos[t] : -1;
   const int base = base0 + st * 64;
   uint4 qf[NS];
   {
-    const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.T * a.H * ROWB));
-    const unsigned qb = (unsigned)(((size_t)t * a.H + head) * ROWB);
+    const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.B * a.T * a.H * ROWB));
+    const unsigned qb = (unsigned)(((size_t)(rb + t) * a.H + head) * ROWB);
     // (tree: waves past the staged sub-tiles may gather, so every wave of a
     // live query tile needs its queries)
     const bool need = TREE ? qt < nqt : work;
@@ -700,7 +720,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
     int pg[NSUB];
     {
       static_assert(NSUB == 4, "one 16-byte load of page numbers");
-      const auto pr = make_rsrc(a.ptable, (unsigned)(a.ptable_len * 4));
+      const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
       const uint4 p4 = bload<0>(pr, (unsigned)((base0 >> 6) * 4));
       pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
     }
@@ -826,15 +846,15 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
     const int pw0 = (base0 >> 6) + g0;
     int pgt[4];
     {
-      const auto pr = make_rsrc(a.ptable, (unsigned)(a.ptable_len * 4));
+      const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
       const unsigned o4 = (unsigned)(pw0 * 4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) pgt[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(pr, o4 + 4 * i, 0, 0);
     }
     // row tr's path (lane j holds the block row at depth j + 1) and position;
     // the next row's are fetched while the current one is computed
-    const auto pathr = make_rsrc(a.path, (unsigned)(a.T * 64));
-    const auto posr = make_rsrc(a.pos, (unsigned)(a.T * 4));
+    const auto pathr = make_rsrc(path, (unsigned)(a.T * 64));
+    const auto posr = make_rsrc(pos, (unsigned)(a.T * 4));
     int tr = t_lo + kk;
     uint32_t pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)(tr * 64 + lane), 0, 0);
     int ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)(tr * 4), 0, 0);
@@ -1002,7 +1022,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < DPT; ++e) O[e] = fmaf(so[e * 17], w, O[e]);
   }
-  float* out = a.part + (((size_t)sp * a.Hkv + gkv) * a.ncols + qcol) * (HD + 2);
+  float* out = a.part + (((size_t)sp * a.Hkv + gkv) * ((size_t)a.B * a.ncols) + (size_t)b * a.ncols + qcol) * (HD + 2);
 #pragma unroll
   for (int e = 0; e < DPT; e += 4)
     *reinterpret_cast<float4*>(out + d0 + e) = make_float4(O[e], O[e + 1], O[e + 2], O[e + 3]);
@@ -1021,8 +1041,10 @@ constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 template <int DT, int HD>
 __global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part,
                                                               const int* __restrict__ info, int max_splits,
-                                                              int Hkv, int G, int ncols, int H,
+                                                              int Hkv, int G, int ncols, int H, int T,
                                                               void* __restrict__ xout, int x_S) {
+  // ncols: query columns of the whole block (all sequences); row t belongs to
+  // sequence t / T
   const int t = blockIdx.x / H, j = blockIdx.x % H;
   const int gkv = j / G, qc = t * G + (j % G);
   const int dim = threadIdx.x * 4;
@@ -1042,7 +1064,7 @@ __global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __res
       os[s] = make_float4(__uint_as_float(ov.x), __uint_as_float(ov.y), __uint_as_float(ov.z), __uint_as_float(ov.w));
     }
   }
-  const int nsplit = info[1];
+  const int nsplit = info[4 * (t / T) + 1];
   float M = -INFINITY;
 #pragma unroll
   for (int s = 0; s < MAX_SPLITS; ++s)
@@ -1098,6 +1120,11 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
                                                     const int* __restrict__ prow,
                                                     const int* __restrict__ greedy, int T, int mode,
                                                     int* __restrict__ result) {
+  // workgroup b: sequence b, rows b*T .. b*T + T - 1, result record b
+  tok += blockIdx.x * T;
+  prow += blockIdx.x * T;
+  greedy += blockIdx.x * T;
+  result += blockIdx.x * (2 + 64);
   const int lane = threadIdx.x;
   const int K = T - 1;
   if (mode == 0) {
@@ -1141,9 +1168,13 @@ template <int DT, int HD>
 __global__ __launch_bounds__(256) void compact_kernel(void* __restrict__ kv_pool, size_t layer_stride,
                                                       const int* __restrict__ ptable,
                                                       const int* __restrict__ result,
-                                                      const int* __restrict__ info, int Hkv) {
+                                                      const int* __restrict__ info, int Hkv,
+                                                      int ptable_len) {
   constexpr int ESZ = Geo<DT>::ESZ;
-  const int n = info[0];
+  // blockIdx.y: sequence
+  ptable += blockIdx.y * ptable_len;
+  result += blockIdx.y * (2 + 64);
+  const int n = info[4 * blockIdx.y];
   const int layer = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
   const int a = result[0];
   unsigned char* lb = reinterpret_cast<unsigned char*>(kv_pool) + layer * layer_stride * ESZ;
@@ -1198,7 +1229,8 @@ int gemm_slices_for(int K, int dt) { return gemm_slices(K / ks_of(dt)); }
 template <int DT, int HD>
 static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   constexpr int KS = Geo<DT>::KS;
-  const int T = s.T, d = m.d, qdim = m.H * m.hd, qkvN = qdim + 2 * m.Hkv * m.hd;
+  const int T = s.T, B = s.B, R = T * B;   // rows per sequence, sequences, rows
+  const int d = m.d, qdim = m.H * m.hd, qkvN = qdim + 2 * m.Hkv * m.hd;
   const int Sd = d / KS, Sq = qdim / KS, Sf = m.F / KS;
   const int sk_d = gemm_slices(Sd), sk_q = gemm_slices(Sq), sk_f = gemm_slices(Sf);
   const size_t layer_elems = (size_t)m.max_pages * 2 * m.Hkv * 64 * m.hd;
@@ -1206,13 +1238,13 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   auto last = [] { return hipGetLastError(); };
 
   if ((e = timed(prof, PC_NORM, st, [&] {
-         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(T), dim3(NORM_THREADS), 0, st, m.embed, w.tok, w.h,
-                            w.part, 1, T, m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
+         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(R), dim3(NORM_THREADS), 0, st, m.embed, w.tok, w.h,
+                            w.part, 1, R, m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
          return last();
        })) != hipSuccess)
     return e;
 
-  const int G = m.H / m.Hkv, ncols = T * G;
+  const int G = m.H / m.Hkv, ncols = T * G;   // query columns per sequence
   const int nsplit = w.max_splits;   // splits beyond the context exit at once
   const int nqt = (ncols + 15) / 16;
   const int pairs = (m.H + 2 * m.Hkv) * (m.hd / 2);
@@ -1221,11 +1253,11 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     const LayerPtrs& lp = m.layers[l];
     void* kvl = reinterpret_cast<unsigned char*>(m.kv_pool) + l * layer_elems * Geo<DT>::ESZ;
     // QKV projection, then rotary + KV append
-    if ((e = timed(prof, PC_QKV, st, [&] { return gemm<DT>(lp.wqkv, w.xbuf, qkvN, d, T, w.part, st); })) != hipSuccess)
+    if ((e = timed(prof, PC_QKV, st, [&] { return gemm<DT>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
-           hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, T), dim3(256), 0, st, w.part,
-                              sk_d, T, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.ptable, w.info, w.q, kvl);
+           hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, R), dim3(256), 0, st, w.part,
+                              sk_d, R, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.slot, w.q, kvl);
            return last();
          })) != hipSuccess)
       return e;
@@ -1233,16 +1265,16 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     AttnArgs aa{};
     aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.path = w.path;
     aa.info = w.info;
-    aa.T = T; aa.H = m.H; aa.Hkv = m.Hkv; aa.G = G; aa.ncols = ncols;
+    aa.T = T; aa.H = m.H; aa.Hkv = m.Hkv; aa.G = G; aa.ncols = ncols; aa.B = B;
     aa.tree = s.mode == 2;
     aa.scale_log2 = 1.4426950408889634f / sqrtf((float)m.hd);
     aa.part = w.attn_part;
     aa.max_pages = m.max_pages;
-    aa.ptable_len = ((m.max_ctx + 63) / 64 + 3) & ~3;
+    aa.ptable_len = w.ptable_len;
     if ((e = timed(prof, PC_ATTN, st, [&] {
            // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
            const int qt = att_qt(aa.tree);
-           const dim3 grid(m.Hkv, nsplit, (nqt + qt - 1) / qt);
+           const dim3 grid(m.Hkv, nsplit, B * ((nqt + qt - 1) / qt));
            if (aa.tree)
              hipLaunchKernelGGL((attn_kernel<DT, HD, true>), grid, dim3(att_threads(true)), 0, st, aa);
            else
@@ -1251,52 +1283,52 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
-           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(T * m.H), dim3(HD / 4), 0, st, w.attn_part,
-                              w.info, w.max_splits, m.Hkv, G, ncols, m.H, (void*)w.xbuf, Sq);
+           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(R * m.H), dim3(HD / 4), 0, st, w.attn_part,
+                              w.info, w.max_splits, m.Hkv, G, R * G, m.H, T, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
       return e;
     // O projection; residual add + FFN norm
-    if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, T, w.part, st); })) != hipSuccess)
+    if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
-                              sk_q, T, lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(R), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
+                              sk_q, R, lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
       return e;
     // gate/up projection, then SwiGLU
-    if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT>(lp.wgu, w.xbuf, 2 * m.F, d, T, w.part, st); })) != hipSuccess)
+    if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
-           hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, T), dim3(256), 0, st, w.part, sk_d,
-                              T, m.F, (void*)w.zbuf, Sf);
+           hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, R), dim3(256), 0, st, w.part, sk_d,
+                              R, m.F, (void*)w.zbuf, Sf);
            return last();
          })) != hipSuccess)
       return e;
     // down projection; residual add + the next norm (layer l+1 attention side, or final)
-    if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT>(lp.wd, w.zbuf, d, m.F, T, w.part, st); })) != hipSuccess)
+    if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT>(lp.wd, w.zbuf, d, m.F, R, w.part, st); })) != hipSuccess)
       return e;
     const float* gn = (l + 1 < m.L) ? m.layers[l + 1].attn_gain : m.final_gain;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(T), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
-                              sk_f, T, gn, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(R), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
+                              sk_f, R, gn, m.eps, d, (void*)w.xbuf, Sd);
            return last();
          })) != hipSuccess)
       return e;
   }
   // LM head, logits + chunk maxima, argmax
-  if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, T, w.part, st); })) != hipSuccess)
+  if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); })) != hipSuccess)
     return e;
   const int nchunk = (m.V + 2047) / 2048;
   if ((e = timed(prof, PC_FINISH, st, [&] {
-         hipLaunchKernelGGL(logits_kernel, dim3(nchunk, T), dim3(256), 0, st, w.part, sk_d, T, m.V, w.logits,
+         hipLaunchKernelGGL(logits_kernel, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V, w.logits,
                             w.amax, nchunk);
          return last();
        })) != hipSuccess)
     return e;
   return timed(prof, PC_ARGMAX, st, [&] {
-    hipLaunchKernelGGL(argmax_kernel, dim3(T), dim3(256), 0, st, w.amax, nchunk, w.greedy);
+    hipLaunchKernelGGL(argmax_kernel, dim3(R), dim3(256), 0, st, w.amax, nchunk, w.greedy);
     return last();
   });
 }
@@ -1311,7 +1343,7 @@ hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof,
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   (void)m;
   return timed(prof, PC_ACCEPT, st, [&] {
-    hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(64), 0, st, w.tok, w.prow, w.greedy, s.T, s.mode,
+    hipLaunchKernelGGL(accept_kernel, dim3(s.B), dim3(64), 0, st, w.tok, w.prow, w.greedy, s.T, s.mode,
                        w.result);
     return hipGetLastError();
   });
@@ -1319,14 +1351,14 @@ hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, 
 
 hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   const size_t layer_elems = (size_t)m.max_pages * 2 * m.Hkv * 64 * m.hd;
-  const dim3 grid(m.L * m.Hkv), block(256);
+  const dim3 grid(m.L * m.Hkv, s.B), block(256);
   return timed(prof, PC_COMPACT, st, [&] {
     if (m.dt == DT_BF16 && m.hd == 128)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
     else if (m.dt == DT_BF16 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
     else if (m.dt == DT_F32 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv);
+      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
     else
       return hipErrorInvalidValue;   // fp32 with head_dim 128 would exceed the LDS staging size
     return hipGetLastError();
