@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
 # The Reuse driver resumes at a match of at least this many generated tokens;
 # shorter (single-token) matches are frequent by chance and can move the
 # cursor past the true position in the original code.
@@ -167,6 +168,49 @@ def other_config(ee, name: str, k: int, ctx: int, reps: int = 60) -> dict:
             "tokens_per_s_full_acceptance": round((k + 1) / p50, 1)}
 
 
+def batch_config(ee, name: str, n_seq: int, k: int, ctx: int, reps: int = 20) -> dict:
+    """Latency of one ee_verify_batch block of n_seq sequences with k-token
+    drafts, every sequence at `ctx` committed positions (rolled back after
+    every step); drafts are each sequence's own next k tokens (all accepted)."""
+    from workloads import gen_weights, get_shape, zipf_tokens
+    shape = get_shape(name)
+    t0 = time.perf_counter()
+    weights = gen_weights(shape, seed=1234, eager=False)   # layers drawn while uploading
+    eng = ee.Engine(shape, weights, max_ctx=ctx + k + 2, max_seqs=n_seq, k_max=k)
+    del weights
+    firsts = [eng.prefill(b, zipf_tokens(shape.vocab, ctx, seed=42 + b)) for b in range(n_seq)]
+    conts = [[eng.verify(b, [])[1] for _ in range(k)] for b in range(n_seq)]
+    setup_s = time.perf_counter() - t0
+    lat = []
+    for i in range(reps + 5):
+        for b in range(n_seq):
+            eng.rollback(b, ctx, firsts[b])
+        ts = time.perf_counter()
+        res = eng.verify_batch(list(range(n_seq)), conts)
+        if i >= 5:
+            lat.append(time.perf_counter() - ts)
+        assert all(a == k for a, _, _ in res)
+    eng.close()
+    p50 = float(np.percentile(lat, 50))
+    one = step_bytes(shape, k + 1, ctx)
+    tb = one["weights"] + n_seq * (one["total"] - one["weights"])
+    rows = n_seq * (k + 1)
+    esz = 2 if shape.dtype == "bf16" else 4
+    flops = 2 * rows * linear_weight_bytes(shape) // esz + n_seq * attention_flops(shape, k + 1, ctx)
+    return {"model": f"{name} Llama-style random-init {shape.dtype}", "sequences": n_seq, "k": k,
+            "ctx": ctx, "rows": rows, "p50_ms": round(p50 * 1e3, 3),
+            "p90_ms": round(float(np.percentile(lat, 90)) * 1e3, 3),
+            "algorithmic_bytes": tb, "hbm_frac": round(tb / p50 / 1e9 / HBM_PEAK_GBS, 4),
+            "flops": flops, "mfma_frac": round(flops / p50 / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "emitted_tokens_per_s": round(n_seq * (k + 1) / p50, 1), "setup_s": round(setup_s, 1)}
+
+
+def attention_flops(s, t: int, n: int) -> int:
+    """Score and value products of t rows over n committed keys plus the
+    block, in every layer."""
+    return s.n_layers * 2 * 2 * s.n_heads * s.head_dim * t * (n + (t + 1) // 2)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -179,6 +223,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
+    ap.add_argument("--no-33b", action="store_true", help="skip the 33B batch-of-4 measurement")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -356,6 +401,9 @@ def main():
     eng.close()
     if args.config == "7b":
         result["other_configs"] = {"1b_k16_ctx1024": other_config(ee, "1b", 16, 1024)}
+        if not args.no_33b:
+            log("[bench] 33B batch of 4 sequences")
+            result["other_configs"]["33b_batch4_k64_ctx4096"] = batch_config(ee, "33b", 4, 64, 4096)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         result["cpu_baseline"] = cpu_baseline(shape, weights, K, ctx, args.cpu_layers,
