@@ -19,6 +19,8 @@ What it computes (all arithmetic in float64):
   of Eq. 7 is greedy) and the longest accepted prefix of Eq. 7, plus the bonus
   token of the all-accepted case (Sec. "Speculative Decoding"); and the
   greedy walk of a draft tree.
+* ``entropy`` - entropy-aware dynamic verification (Eq. 9-10) and fixed
+  top-k verification of draft-model tokens (Sec. "Edit").
 * ``match`` - the prefix/suffix matcher that resumes Reuse (Sec. "Reuse").
 * ``session`` - prefill / verify / rollback / plain greedy decoding (Eq. 1)
   over an oracle-owned KV cache.
@@ -27,11 +29,13 @@ What it computes (all arithmetic in float64):
 from .numerics import round_bf16
 from .model import forward_block, chain_structure, tree_structure
 from .accept import greedy_rows, accept_linear, accept_tree, top2_margin
+from .entropy import accept_topk, entropy_threshold, topk_tokens
 from .match import match_reuse
 from .session import OracleSession
 
 __all__ = [
     "round_bf16", "forward_block", "chain_structure", "tree_structure",
     "greedy_rows", "accept_linear", "accept_tree", "top2_margin", "match_reuse",
+    "accept_topk", "entropy_threshold", "topk_tokens",
     "OracleSession",
 ]
