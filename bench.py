@@ -340,6 +340,39 @@ def main():
     l50, l90, acc = fixed_ctx(ttoks, parent)
     tree64 = dict(lat_entry(64, l50, l90, acc), nodes=64, max_depth=8, max_branch=3)
 
+    # entropy-aware dynamic and fixed top-k verification (Eq. 9-10) on the
+    # same draft as the headline latency, with the per-class time of the
+    # kernels that differ from greedy verification (logits epilogue, selection)
+    def topk_ctx(draft, k, dynamic, reps=60):
+        lat, acc = [], []
+        for i in range(reps):
+            eng.rollback(0, ctx, first)
+            ts = time.perf_counter()
+            (a, _, _), = eng.verify_topk([0], [draft], k, dynamic)
+            if i >= 10:
+                lat.append(time.perf_counter() - ts)
+                acc.append(a)
+        return float(np.percentile(lat, 50)), float(np.percentile(lat, 90)), float(np.mean(acc))
+
+    def select_ms(fn):
+        eng.profile(["finish", "argmax"])
+        eng.profile_read(reset=True)
+        for _ in range(10):
+            eng.rollback(0, ctx, first)
+            fn()
+        pr = eng.profile_read(reset=True)
+        eng.profile([])
+        return {c: round(ms / 10, 4) for c, (ms, n) in pr.items() if n}
+    d_topk = code[1:1 + K]
+    entropy = {"k_draft": K, "draft": "the headline draft (edited copy of the greedy output)"}
+    for kk, dyn in ((5, True), (3, True), (5, False)):
+        l50, l90, acc = topk_ctx(d_topk, kk, dyn)
+        entropy[f"{'dynamic' if dyn else 'fixed'}_top{kk}"] = {
+            "p50_ms": round(l50 * 1e3, 4), "p90_ms": round(l90 * 1e3, 4), "accepted": round(acc, 2)}
+    entropy["per_step_ms_topk5_dynamic"] = select_ms(lambda: eng.verify_topk([0], [d_topk], 5, True))
+    entropy["per_step_ms_greedy"] = select_ms(lambda: eng.verify(0, d_topk))
+    eng.rollback(0, ctx, first)
+
     # a plain device copy of known size, so that hardware byte counters read on
     # this run can be scaled against it
     cal = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
@@ -396,6 +429,7 @@ def main():
         "breakdown_ms_per_step": brk,
         "k_sweep_at_ctx": k_sweep,
         "tree64_at_ctx": tree64,
+        "entropy_verify_at_ctx": entropy,
         "lossless_check": "emitted stream equals the GPU's own greedy output",
     }
     eng.close()

@@ -142,6 +142,27 @@ int32_t ee_verify_batch(ee_ctx* ctx, int32_t n_seq, const int32_t* seqs, const i
                         int32_t K, const int32_t* parents, int32_t* accept_lens,
                         int32_t* next_tokens, int32_t* accepted_nodes);
 
+/* Entropy-aware dynamic verification (Sec. "Edit", Eq. 9-10) and its fixed
+ * top-k variant, for linear drafts of n_seq distinct sequences (layout of
+ * seqs, drafts, accept_lens and next_tokens as in ee_verify_batch).
+ * For every block row i < K of a sequence, the target's top_k tokens are
+ * ranked by logit (ties: lower token id first) and their probabilities
+ * renormalised over those top_k tokens give the normalised entropy
+ * H_i = -sum q log q / log(top_k), computed in float64 from the float32
+ * logits.  The threshold is tau_i = max(1, ceil(top_k * H_i)) when dynamic
+ * != 0, else top_k (top_k == 1 gives tau = 1: plain greedy verification).
+ * Draft token d_{i+1} is accepted when it is one of row i's first tau_i
+ * tokens; accept_len a = the longest accepted prefix, next_token = the greedy
+ * (top-1) token of row a.  Unlike greedy verification this accepts tokens
+ * other than the target's own, so the output may differ from plain greedy
+ * decoding.  thresholds (optional, room for n_seq * K) receives tau_i of
+ * every draft row at thresholds[b*K + i].
+ * Effects, atomicity and errors: as ee_verify_batch, plus EE_EINVAL for
+ * top_k outside [1, min(8, vocab)]. */
+int32_t ee_verify_topk(ee_ctx* ctx, int32_t n_seq, const int32_t* seqs, const int32_t* drafts,
+                       int32_t K, int32_t top_k, int32_t dynamic, int32_t* accept_lens,
+                       int32_t* next_tokens, int32_t* thresholds);
+
 /* Truncate sequence `seq` to its first new_len committed positions
  * (new_len <= len), release pages wholly beyond them and make pending_token
  * pending.  new_len == 0 with pending_token == -1 empties the sequence (it

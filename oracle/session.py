@@ -9,6 +9,9 @@ Conventions (the paper leaves them open):
   pointers), accepts by Eq. 7 / the tree walk, commits the pending row plus
   the accepted rows in depth order (n -> n + 1 + a) and makes the emitted
   next token pending.  K = 0 is one plain greedy step of Eq. 1.
+* ``verify_topk`` is ``verify`` of a chain with the entropy-aware (or fixed)
+  top-k acceptance of Eq. 9-10 in place of Eq. 7; ``score`` returns the
+  logits of a chain block without committing anything.
 * ``rollback`` truncates the committed cache to a shorter length and sets a
   new pending token.
 """
@@ -18,6 +21,7 @@ from __future__ import annotations
 import numpy as np
 
 from .accept import accept_linear, accept_tree, greedy_rows
+from .entropy import accept_topk
 from .model import chain_structure, forward_block, tree_structure
 
 
@@ -73,6 +77,28 @@ class OracleSession:
         self.pending = nxt
         self.last_logits = logits
         return a, nxt, path
+
+    def score(self, draft):
+        """Logits of the chain [pending, d_1..d_K]; the cache is unchanged."""
+        tokens = np.concatenate([[self.pending], np.asarray(draft, dtype=np.int64)])
+        depth, vis = chain_structure(len(tokens))
+        logits, _ = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis)
+        return logits
+
+    def verify_topk(self, draft, k: int, dynamic: bool = True):
+        """Chain verification with the top-k acceptance of Eq. 9-10.
+        Returns (accept_len, next_token, thresholds of the checked rows)."""
+        if self.pending is None:
+            raise RuntimeError("verify before prefill")
+        draft = np.asarray(draft, dtype=np.int64)
+        tokens = np.concatenate([[self.pending], draft])
+        depth, vis = chain_structure(len(tokens))
+        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis)
+        a, nxt, taus = accept_topk(draft, logits, k, dynamic)
+        self._commit(blk, list(range(a + 1)))
+        self.pending = nxt
+        self.last_logits = logits
+        return a, nxt, taus
 
     def greedy(self, steps: int):
         """Plain token-by-token greedy decoding (Eq. 1); returns emitted tokens."""

@@ -60,6 +60,7 @@ ee_destroy = _sig("ee_destroy", _i32, [_vp])
 ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_batch = _sig("ee_verify_batch", _i32, [_vp, _i32, _pi32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
+ee_verify_topk = _sig("ee_verify_topk", _i32, [_vp, _i32, _pi32, _pi32, _i32, _i32, _i32, _pi32, _pi32, _pi32])
 ee_kv_rollback = _sig("ee_kv_rollback", _i32, [_vp, _i32, _i32, _i32])
 ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
 ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32, _i32, _i32, _pi32, _pi32])
@@ -219,6 +220,26 @@ class Engine:
             a = int(acc[b])
             out.append((a, int(nxt[b]), nodes[b * k:b * k + a].copy() if parents is not None else None))
         return out
+
+    def verify_topk(self, seqs, drafts, top_k: int, dynamic: bool = True):
+        """Entropy-aware (``dynamic``) or fixed top-k verification of linear
+        drafts, one per sequence, all of the same length.  Returns
+        [(accept_len, next_token, thresholds)] in the order of ``seqs``, where
+        thresholds[i] is the tau applied to draft token i."""
+        n = len(seqs)
+        k = len(drafts[0]) if n else 0
+        if len(drafts) != n or any(len(d) != k for d in drafts):
+            raise EEError(EE_EINVAL, "one draft per sequence, all of the same length")
+        sq, sp = _i32arr(seqs)
+        d, dp = _i32arr(np.concatenate([np.asarray(x, dtype=np.int32).reshape(-1) for x in drafts])
+                        if n else np.zeros(0, np.int32))
+        acc = np.zeros(max(n, 1), dtype=np.int32)
+        nxt = np.zeros(max(n, 1), dtype=np.int32)
+        thr = np.zeros(max(n * k, 1), dtype=np.int32)
+        _check(ee_verify_topk(self.ctx, n, sp, dp, k, int(top_k), int(bool(dynamic)), acc.ctypes.data_as(_pi32),
+                              nxt.ctypes.data_as(_pi32), thr.ctypes.data_as(_pi32)), self.ctx)
+        self._last_rows = n * (k + 1)
+        return [(int(acc[b]), int(nxt[b]), thr[b * k:(b + 1) * k].copy()) for b in range(n)]
 
     def rollback(self, seq: int, new_len: int, pending: int):
         _check(ee_kv_rollback(self.ctx, seq, new_len, pending), self.ctx)

@@ -41,7 +41,7 @@ struct Layout {
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
-  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, result, stage, rope, ws_total;
+  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
   size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, stage_bytes;
   size_t kv_layer, kv_total;
@@ -130,8 +130,9 @@ Layout make_layout(const ee_model_config* c) {
     L.gpart = o; o += up(mx * L.Rmax * 4);
   }
   L.logits = o; o += up(L.Rmax * V * 4);
-  L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8);
+  L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8 * 8);
   L.greedy = o; o += up(L.Rmax * 4);
+  L.verdict = o; o += up(L.Rmax * 4);
   L.result = o; o += up((size_t)c->max_seqs * (2 + 64) * 4);
   // staging block: one host->device copy per call
   size_t so = 0;
@@ -219,6 +220,7 @@ void bind_work(ee_ctx* c) {
   w.logits = reinterpret_cast<float*>(ws + L.logits);
   w.amax = reinterpret_cast<unsigned long long*>(ws + L.amax);
   w.greedy = reinterpret_cast<int*>(ws + L.greedy);
+  w.verdict = reinterpret_cast<int*>(ws + L.verdict);
   w.result = reinterpret_cast<int*>(ws + L.result);
   unsigned char* sb = ws + L.stage;
   w.path = sb + L.s_path;
@@ -303,8 +305,9 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
 // Stage the per-sequence state (page tables, committed lengths, the KV slot
 // of every row), run the forward + acceptance (+ tree compaction) of B
 // sequences of T rows whose tokens, positions and parents the caller staged,
-// and fetch the results (record b at h_result + b * (2 + 64)).
-int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode) {
+// and fetch the results (record b at h_result + b * (2 + 64)).  Mode 3 uses
+// the top-k size and dynamic flag given for every sequence.
+int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0, int dynamic = 0) {
   const Layout& L = c->lay;
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
   int* info = reinterpret_cast<int*>(c->h_stage + L.s_info);
@@ -314,6 +317,8 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode) {
     for (size_t i = 0; i < s.pages.size(); ++i) ptab[b * L.ptable_len + i] = s.pages[i];
     info[4 * b + 0] = s.len;
     info[4 * b + 1] = (s.len + T + SPLIT - 1) / SPLIT;
+    info[4 * b + 2] = top_k;
+    info[4 * b + 3] = dynamic;
     for (int t = 0; t < T; ++t) {
       const int p = s.len + t;   // block row t lands in slot len + t
       slot[b * T + t] = s.pages[p / PAGE] * PAGE + p % PAGE;
@@ -386,6 +391,65 @@ void stage_draft(ee_ctx* c, int b, int T, const Seq& s, const int32_t* draft, co
       pos[r] = s.len + r;
     }
   }
+}
+
+// One block of n_seq sequences with K draft tokens each: greedy (top_k 0;
+// linear, or trees when `parents` is given) or top-k verification (top_k >= 1,
+// linear).  Everything is validated and every page reserved before anything
+// runs, so an error leaves every sequence as it was.
+int verify_many(ee_ctx* c, int n_seq, const int32_t* seqs, const int32_t* drafts, int K, const int32_t* parents,
+                int top_k, int dynamic, int32_t* accept_lens, int32_t* next_tokens, int32_t* accepted_nodes,
+                int32_t* thresholds) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (n_seq < 1 || n_seq > c->cfg.max_seqs) return fail(c, EE_EINVAL, "n_seq outside [1, max_seqs]");
+  if (!seqs || !accept_lens || !next_tokens)
+    return fail(c, EE_EINVAL, "seqs, accept_lens and next_tokens must be non-NULL");
+  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
+  const int T = K + 1;
+  std::vector<int> depth((size_t)n_seq * 65);
+  std::vector<Seq*> ss(n_seq);
+  for (int b = 0; b < n_seq; ++b) {
+    int rc = check_seq(c, seqs[b]);
+    if (rc) return rc;
+    for (int b2 = 0; b2 < b; ++b2)
+      if (seqs[b2] == seqs[b]) return fail(c, EE_EINVAL, "a sequence appears twice in the batch");
+    Seq& s = c->seqs[seqs[b]];
+    if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
+    if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
+    if ((rc = check_draft(c, drafts ? drafts + (size_t)b * K : nullptr, K,
+                          parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65])))
+      return rc;
+    ss[b] = &s;
+  }
+  std::vector<int> added(n_seq, 0);
+  for (int b = 0; b < n_seq; ++b) {
+    if (!reserve_pages(c, *ss[b], ss[b]->len + T, &added[b])) {
+      for (int b2 = 0; b2 <= b; ++b2) unreserve(c, *ss[b2], added[b2]);
+      return fail(c, EE_ECAPACITY, "KV pool exhausted");
+    }
+  }
+  for (int b = 0; b < n_seq; ++b)
+    stage_draft(c, b, T, *ss[b], drafts ? drafts + (size_t)b * K : nullptr,
+                parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65]);
+  const int mode = top_k ? 3 : (parents ? 2 : 1);
+  const int rc = run_block(c, ss.data(), n_seq, T, mode, top_k, dynamic);
+  if (rc) {
+    for (int b = 0; b < n_seq; ++b) unreserve(c, *ss[b], added[b]);
+    return rc;
+  }
+  for (int b = 0; b < n_seq; ++b) {
+    const int* res = c->h_result + (size_t)b * (2 + 64);
+    const int a = res[0];
+    ss[b]->len += 1 + a;
+    ss[b]->pending = res[1];
+    accept_lens[b] = a;
+    next_tokens[b] = res[1];
+    if (accepted_nodes)
+      for (int i = 0; i < a; ++i) accepted_nodes[(size_t)b * K + i] = res[2 + i] - 1;
+    if (thresholds)
+      for (int i = 0; i < K; ++i) thresholds[(size_t)b * K + i] = res[2 + i];
+  }
+  return EE_OK;
 }
 
 }  // namespace
@@ -611,53 +675,16 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
 int32_t ee_verify_batch(ee_ctx* c, int32_t n_seq, const int32_t* seqs, const int32_t* drafts, int32_t K,
                         const int32_t* parents, int32_t* accept_lens, int32_t* next_tokens,
                         int32_t* accepted_nodes) {
+  return verify_many(c, n_seq, seqs, drafts, K, parents, 0, 0, accept_lens, next_tokens, accepted_nodes, nullptr);
+}
+
+int32_t ee_verify_topk(ee_ctx* c, int32_t n_seq, const int32_t* seqs, const int32_t* drafts, int32_t K,
+                       int32_t top_k, int32_t dynamic, int32_t* accept_lens, int32_t* next_tokens,
+                       int32_t* thresholds) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
-  if (n_seq < 1 || n_seq > c->cfg.max_seqs) return fail(c, EE_EINVAL, "n_seq outside [1, max_seqs]");
-  if (!seqs || !accept_lens || !next_tokens)
-    return fail(c, EE_EINVAL, "seqs, accept_lens and next_tokens must be non-NULL");
-  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
-  const int T = K + 1;
-  std::vector<int> depth((size_t)n_seq * 65);
-  std::vector<Seq*> ss(n_seq);
-  for (int b = 0; b < n_seq; ++b) {
-    int rc = check_seq(c, seqs[b]);
-    if (rc) return rc;
-    for (int b2 = 0; b2 < b; ++b2)
-      if (seqs[b2] == seqs[b]) return fail(c, EE_EINVAL, "a sequence appears twice in the batch");
-    Seq& s = c->seqs[seqs[b]];
-    if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
-    if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
-    if ((rc = check_draft(c, drafts ? drafts + (size_t)b * K : nullptr, K,
-                          parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65])))
-      return rc;
-    ss[b] = &s;
-  }
-  std::vector<int> added(n_seq, 0);
-  for (int b = 0; b < n_seq; ++b) {
-    if (!reserve_pages(c, *ss[b], ss[b]->len + T, &added[b])) {
-      for (int b2 = 0; b2 <= b; ++b2) unreserve(c, *ss[b2], added[b2]);
-      return fail(c, EE_ECAPACITY, "KV pool exhausted");
-    }
-  }
-  for (int b = 0; b < n_seq; ++b)
-    stage_draft(c, b, T, *ss[b], drafts ? drafts + (size_t)b * K : nullptr,
-                parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65]);
-  const int rc = run_block(c, ss.data(), n_seq, T, parents ? 2 : 1);
-  if (rc) {
-    for (int b = 0; b < n_seq; ++b) unreserve(c, *ss[b], added[b]);
-    return rc;
-  }
-  for (int b = 0; b < n_seq; ++b) {
-    const int* res = c->h_result + (size_t)b * (2 + 64);
-    const int a = res[0];
-    ss[b]->len += 1 + a;
-    ss[b]->pending = res[1];
-    accept_lens[b] = a;
-    next_tokens[b] = res[1];
-    if (accepted_nodes)
-      for (int i = 0; i < a; ++i) accepted_nodes[(size_t)b * K + i] = res[2 + i] - 1;
-  }
-  return EE_OK;
+  if (top_k < 1 || top_k > 8 || top_k > c->cfg.vocab) return fail(c, EE_EINVAL, "top_k outside [1, min(8, vocab)]");
+  return verify_many(c, n_seq, seqs, drafts, K, nullptr, top_k, dynamic ? 1 : 0, accept_lens, next_tokens,
+                     nullptr, thresholds);
 }
 
 int32_t ee_kv_rollback(ee_ctx* c, int32_t seq, int32_t new_len, int32_t pending_token) {

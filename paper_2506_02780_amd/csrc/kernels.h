@@ -67,8 +67,9 @@ struct Work {
   float* attn_part;         // [splits][Hkv][Rmax*G][hd + 2]
   float* part;              // GEMM slice partials [SK][R][N]
   float* logits;            // [Rmax, V]
-  unsigned long long* amax; // [Rmax, ceil(V/2048)]
+  unsigned long long* amax; // [Rmax, ceil(V/2048), 8] chunk maxima (top-8 in mode 3)
   int* greedy;              // [Rmax]
+  int* verdict;             // [Rmax] mode 3: tau | draft-accepted << 8
   int* result;              // [max_seqs][2 + 64]: accept_len, next, accepted rows
   // staged per call (host -> device)
   int* tok;                 // [Rmax]
@@ -78,7 +79,8 @@ struct Work {
   unsigned char* path;      // [Rmax][64] tree mode: entry j-1 of row t = block row at
                             // depth j on t's path (row 0, the pending token, is depth 0)
   int* ptable;              // [max_seqs][ptable_len] page of each 64-position block
-  int* info;                // [max_seqs][4]: committed positions n, attention splits in use
+  int* info;                // [max_seqs][4]: committed positions n, attention splits in use,
+                            // top-k size k and dynamic flag (mode 3)
   int ptable_len;           // entries per sequence (multiple of 4)
   int max_splits;           // attention splits of the longest context
 };
@@ -101,7 +103,7 @@ struct Prof {
 struct Step {
   int T;        // rows per sequence
   int B;        // sequences in the block
-  int mode;     // 0 prefill, 1 linear verify, 2 tree verify
+  int mode;     // 0 prefill, 1 linear verify, 2 tree verify, 3 linear top-k verify
 };
 
 enum ProfClass {

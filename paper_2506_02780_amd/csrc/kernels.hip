@@ -474,32 +474,95 @@ __device__ __forceinline__ unsigned long long amax_key(float v, int idx) {
   return ((unsigned long long)ord << 32) | (0xffffffffu - (uint32_t)idx);
 }
 
+// Descending compare-exchange of two keys.
+__device__ __forceinline__ void cx_desc(unsigned long long& a, unsigned long long& b) {
+  const unsigned long long hi = a > b ? a : b, lo = a > b ? b : a;
+  a = hi;
+  b = lo;
+}
+
+// Sort 8 keys into descending order (Batcher's odd-even merge network).
+__device__ __forceinline__ void sort8_desc(unsigned long long (&k)[8]) {
+  cx_desc(k[0], k[1]); cx_desc(k[2], k[3]); cx_desc(k[4], k[5]); cx_desc(k[6], k[7]);
+  cx_desc(k[0], k[2]); cx_desc(k[1], k[3]); cx_desc(k[4], k[6]); cx_desc(k[5], k[7]);
+  cx_desc(k[1], k[2]); cx_desc(k[5], k[6]);
+  cx_desc(k[0], k[4]); cx_desc(k[1], k[5]); cx_desc(k[2], k[6]); cx_desc(k[3], k[7]);
+  cx_desc(k[2], k[4]); cx_desc(k[3], k[5]);
+  cx_desc(k[1], k[2]); cx_desc(k[3], k[4]); cx_desc(k[5], k[6]);
+}
+
+// The 8 largest keys held by a wave whose lanes each hold a descending list
+// of 8.  Keys are distinct (the column index is part of the key) except 0,
+// which stands for "no element"; every lane receives the same result.
+__device__ __forceinline__ void wave_top8(unsigned long long (&k)[8], unsigned long long (&out)[8]) {
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    unsigned long long m = k[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const unsigned long long x = __shfl_xor(m, o);
+      m = x > m ? x : m;
+    }
+    out[r] = m;
+    const bool pop = m != 0ull && k[0] == m;
+#pragma unroll
+    for (int i = 0; i < 7; ++i) k[i] = pop ? k[i + 1] : k[i];
+    k[7] = pop ? 0ull : k[7];
+  }
+}
+
+// Logits of row t from the LM-head partials, plus, per 2048-column chunk,
+// either the largest key (TOPK false: amax[t][chunk]) or the 8 largest keys
+// in descending order (TOPK true: amax[t][chunk][8]).
+template <bool TOPK>
 __global__ __launch_bounds__(256) void logits_kernel(const float* __restrict__ part, int SK, int T, int V,
                                                      float* __restrict__ logits,
                                                      unsigned long long* __restrict__ amax, int nchunk) {
-  __shared__ unsigned long long sh[256];
   const int t = blockIdx.y;
   const int col = (blockIdx.x * 256 + threadIdx.x) * 8;
-  unsigned long long best = 0;
-  if (col < V) {
+  unsigned long long key[8] = {0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull};
+  if (col < V) {   // V is a multiple of 16: a thread's 8 columns are all in range or all out
     const float4 a = sum_slices4(part, SK, T, V, t, col), b = sum_slices4(part, SK, T, V, t, col + 4);
     float* lr = logits + (size_t)t * V + col;
     *reinterpret_cast<float4*>(lr) = a;
     *reinterpret_cast<float4*>(lr + 4) = b;
     const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const unsigned long long kk = amax_key(v[e], col + e);
-      best = kk > best ? kk : best;
+    for (int e = 0; e < 8; ++e) key[e] = amax_key(v[e], col + e);
+  }
+  if constexpr (!TOPK) {
+    __shared__ unsigned long long sh[256];
+    unsigned long long best = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) best = key[e] > best ? key[e] : best;
+    sh[threadIdx.x] = best;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if ((int)threadIdx.x < w && sh[threadIdx.x + w] > sh[threadIdx.x]) sh[threadIdx.x] = sh[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) amax[(size_t)t * nchunk + blockIdx.x] = sh[0];
+  } else {
+    __shared__ unsigned long long sh[4][8];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    unsigned long long top[8];
+    sort8_desc(key);
+    wave_top8(key, top);
+    if (lane == 0) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sh[wv][i] = top[i];
+    }
+    __syncthreads();
+    if (wv == 0) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) key[i] = lane < 4 ? sh[lane & 3][i] : 0ull;
+      wave_top8(key, top);
+      unsigned long long mine = 0ull;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) mine = lane == i ? top[i] : mine;
+      if (lane < 8) amax[((size_t)t * nchunk + blockIdx.x) * 8 + lane] = mine;
     }
   }
-  sh[threadIdx.x] = best;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w && sh[threadIdx.x + w] > sh[threadIdx.x]) sh[threadIdx.x] = sh[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) amax[(size_t)t * nchunk + blockIdx.x] = sh[0];
 }
 
 // --------------------------------------------------------------- attention --
@@ -1114,11 +1177,83 @@ __global__ __launch_bounds__(256) void argmax_kernel(const unsigned long long* _
   if (threadIdx.x == 0) greedy[t] = (int)(0xffffffffu - (uint32_t)(sh[0] & 0xffffffffull));
 }
 
+// Value of an ordered key (inverse of amax_key; -0 comes back as +0).
+__device__ __forceinline__ float key_value(unsigned long long key) {
+  const uint32_t ord = (uint32_t)(key >> 32);
+  return __uint_as_float((ord & 0x80000000u) ? (ord & 0x7fffffffu) : ~ord);
+}
+__device__ __forceinline__ int key_index(unsigned long long key) {
+  return (int)(0xffffffffu - (uint32_t)(key & 0xffffffffull));
+}
+
+// Entropy-aware top-k verification of row t (Eq. 9-10), one wave per row.
+// The row's top-k tokens (k = info[4b+2] <= 8, ties ranked by lower id) come
+// from merging the per-chunk top-8 keys; their probabilities renormalised
+// over the k tokens give the normalised entropy H = -sum q log q / log k, in
+// float64, and the threshold tau = max(1, ceil(k H)) (dynamic, info[4b+3] != 0)
+// or tau = k (fixed).  The draft token of row t + 1 is accepted when it is one
+// of the first tau tokens.  verdict[t] = tau | accepted << 8; greedy[t] is the
+// top-1 token, i.e. the greedy token of the row.
+__global__ __launch_bounds__(64) void topk_select_kernel(const unsigned long long* __restrict__ cand, int nchunk,
+                                                         const int* __restrict__ tok,
+                                                         const int* __restrict__ info, int T,
+                                                         int* __restrict__ greedy, int* __restrict__ verdict) {
+  const int t = blockIdx.x, lane = threadIdx.x;
+  const int b = t / T, tt = t - b * T;
+  unsigned long long k8[8] = {0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull}, top[8];
+  const unsigned long long* row = cand + (size_t)t * nchunk * 8;
+  for (int i = lane; i < nchunk * 8; i += 64) {
+    const unsigned long long x = row[i];
+    if (x > k8[7]) {
+      k8[7] = x;
+#pragma unroll
+      for (int j = 7; j > 0; --j) cx_desc(k8[j - 1], k8[j]);
+    }
+  }
+  wave_top8(k8, top);
+  const int kk = info[4 * b + 2], dyn = info[4 * b + 3];
+  int tau = kk;
+  if (kk > 1) {
+    const double v0 = (double)key_value(top[0]);
+    double e[8], S = 0.0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      e[j] = (j < kk && top[j] != 0ull) ? exp((double)key_value(top[j]) - v0) : 0.0;
+      S += e[j];
+    }
+    double hs = 0.0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const double q = e[j] / S;
+      if (q > 0.0) hs += q * log(q);
+    }
+    const double H = -hs / log((double)kk);
+    if (dyn) {
+      const double up = ceil((double)kk * H);
+      tau = up < 1.0 ? 1 : (up > (double)kk ? kk : (int)up);
+    }
+  } else {
+    tau = 1;
+  }
+  int hit = 0;
+  if (tt + 1 < T) {
+    const int d = tok[t + 1];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) hit |= (j < tau && top[j] != 0ull && key_index(top[j]) == d) ? 1 : 0;
+  }
+  if (lane == 0) {
+    greedy[t] = key_index(top[0]);
+    verdict[t] = tau | (hit << 8);
+  }
+}
+
 // result[0] = accepted rows a, result[1] = next token, result[2..2+a) = accepted
-// block rows in depth order.  Mode 0 (prefill) commits every row.
+// block rows in depth order (mode 3: result[2..2+K) = the threshold tau of
+// every draft row).  Mode 0 (prefill) commits every row.
 __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
                                                     const int* __restrict__ prow,
-                                                    const int* __restrict__ greedy, int T, int mode,
+                                                    const int* __restrict__ greedy,
+                                                    const int* __restrict__ verdict, int T, int mode,
                                                     int* __restrict__ result) {
   // workgroup b: sequence b, rows b*T .. b*T + T - 1, result record b
   tok += blockIdx.x * T;
@@ -1132,6 +1267,19 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
       result[0] = T - 1;
       result[1] = greedy[T - 1];
     }
+    return;
+  }
+  if (mode == 3) {
+    // draft d_{i+1} passes when row i's verdict accepted it; result[2+i] = tau of row i
+    verdict += blockIdx.x * T;
+    const int vd = lane < K ? verdict[lane] : 0;
+    const unsigned long long b = __ballot(lane < K && !((vd >> 8) & 1));
+    const int a = b ? __ffsll((long long)b) - 1 : K;
+    if (lane == 0) {
+      result[0] = a;
+      result[1] = greedy[a];
+    }
+    if (lane < K) result[2 + lane] = vd & 0xff;
     return;
   }
   if (mode == 1) {
@@ -1321,14 +1469,23 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); })) != hipSuccess)
     return e;
   const int nchunk = (m.V + 2047) / 2048;
+  const bool topk = s.mode == 3;
   if ((e = timed(prof, PC_FINISH, st, [&] {
-         hipLaunchKernelGGL(logits_kernel, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V, w.logits,
-                            w.amax, nchunk);
+         if (topk)
+           hipLaunchKernelGGL(logits_kernel<true>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
+                              w.logits, w.amax, nchunk);
+         else
+           hipLaunchKernelGGL(logits_kernel<false>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
+                              w.logits, w.amax, nchunk);
          return last();
        })) != hipSuccess)
     return e;
   return timed(prof, PC_ARGMAX, st, [&] {
-    hipLaunchKernelGGL(argmax_kernel, dim3(R), dim3(256), 0, st, w.amax, nchunk, w.greedy);
+    if (topk)
+      hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(64), 0, st, w.amax, nchunk, w.tok, w.info, s.T,
+                         w.greedy, w.verdict);
+    else
+      hipLaunchKernelGGL(argmax_kernel, dim3(R), dim3(256), 0, st, w.amax, nchunk, w.greedy);
     return last();
   });
 }
@@ -1343,8 +1500,8 @@ hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof,
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   (void)m;
   return timed(prof, PC_ACCEPT, st, [&] {
-    hipLaunchKernelGGL(accept_kernel, dim3(s.B), dim3(64), 0, st, w.tok, w.prow, w.greedy, s.T, s.mode,
-                       w.result);
+    hipLaunchKernelGGL(accept_kernel, dim3(s.B), dim3(64), 0, st, w.tok, w.prow, w.greedy, w.verdict, s.T,
+                       s.mode, w.result);
     return hipGetLastError();
   });
 }

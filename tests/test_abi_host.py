@@ -54,6 +54,8 @@ def test_null_context_calls_fail_cleanly():
     a = ctypes.c_int32()
     assert ee.ee_verify(None, 0, None, 0, None, ctypes.byref(a), ctypes.byref(a), None) == ee.EE_EINVAL
     assert ee.ee_kv_rollback(None, 0, 0, 0) == ee.EE_EINVAL
+    assert ee.ee_verify_batch(None, 1, None, None, 0, None, None, None, None) == ee.EE_EINVAL
+    assert ee.ee_verify_topk(None, 1, None, None, 0, 3, 1, None, None, None) == ee.EE_EINVAL
 
 
 def test_matcher_equals_oracle():
