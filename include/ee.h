@@ -52,7 +52,7 @@ typedef struct ee_ctx ee_ctx;
  * biases, untied LM head).  Requirements checked by ee_create:
  *   head_dim in {64, 128} (64 for EE_F32); n_heads % n_kv_heads == 0;
  *   d_model, ffn, n_heads*head_dim and vocab multiples of 32 (bf16) or 16 (f32);
- *   page_size == 64; 0 <= k_max <= 64; 1 <= max_ctx <= 8192; max_seqs >= 1. */
+ *   page_size == 64; 0 <= k_max <= 512; 1 <= max_ctx <= 8192; max_seqs >= 1. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn, vocab;
   int32_t dtype;        /* EE_F32 or EE_BF16: weights, KV cache, GEMM inputs */
@@ -60,7 +60,7 @@ typedef struct {
   float rope_theta;     /* rotary base                                        */
   int32_t max_ctx;      /* longest sequence (committed + one block)          */
   int32_t max_seqs;     /* sequences that may be live at once                */
-  int32_t k_max;        /* largest draft (linear length or tree node count)  */
+  int32_t k_max;        /* longest draft (linear; draft trees <= 64 nodes)   */
   int32_t page_size;    /* KV positions per page                              */
 } ee_model_config;
 
@@ -110,7 +110,7 @@ int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
  *   parent == NULL: linear chain; accept_len = largest a with d_i equal to
  *     the greedy token of row i-1 for all i <= a; next_token = greedy token of
  *     row a (the correction after a rejection, the bonus token if a == K).
- *   parent != NULL: draft tree of K nodes; parent[i] is the node that node i
+ *   parent != NULL: draft tree of K <= 64 nodes; parent[i] is the node that node i
  *     extends (-1 = the pending token) and must satisfy parent[i] < i; node i
  *     sees the committed cache, the pending row and its ancestors.  Greedy
  *     walk: from the pending row, step to the lowest-indexed child whose token
@@ -121,7 +121,7 @@ int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
  * 1 + accept_len, tree rows compacted to depth order), next_token becomes
  * pending.  K = 0 is exactly one plain greedy decoding step (Eq. 1).
  * Errors: EE_ESTATE before prefill; EE_EINVAL for K < 0, K > k_max, a token
- * outside [0, vocab) or a malformed tree; EE_ECAPACITY if len + K + 1 would
+ * outside [0, vocab), a malformed tree or a tree of more than 64 nodes; EE_ECAPACITY if len + K + 1 would
  * exceed max_ctx or the KV pool has no free page. */
 int32_t ee_verify(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t K,
                   const int32_t* parent, int32_t* accept_len, int32_t* next_token,

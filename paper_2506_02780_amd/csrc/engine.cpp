@@ -21,6 +21,8 @@ namespace {
 
 constexpr int PAGE = 64;
 constexpr int SPLIT = 256;
+constexpr int MAX_K = 512;        // longest linear draft
+constexpr int MAX_TREE = 64;      // largest draft tree (one node per lane of a wave)
 constexpr size_t ALIGN = 256;
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
@@ -63,7 +65,7 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   if (c->d_model % ks || c->ffn % ks || (c->n_heads * c->head_dim) % ks || c->vocab % ks)
     return bad("d_model, ffn, n_heads*head_dim and vocab must be multiples of 32 (bf16) / 16 (f32)");
   if (c->page_size != PAGE) return bad("page_size must be 64");
-  if (c->k_max < 0 || c->k_max > 64) return bad("k_max must be in [0, 64]");
+  if (c->k_max < 0 || c->k_max > MAX_K) return bad("k_max must be in [0, 512]");
   if (c->max_ctx < 1 || c->max_seqs < 1) return bad("max_ctx and max_seqs must be positive");
   if (c->max_ctx > 8192) return bad("max_ctx must be at most 8192");
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0");
@@ -133,7 +135,7 @@ Layout make_layout(const ee_model_config* c) {
   L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8 * 8);
   L.greedy = o; o += up(L.Rmax * 4);
   L.verdict = o; o += up(L.Rmax * 4);
-  L.result = o; o += up((size_t)c->max_seqs * (2 + 64) * 4);
+  L.result = o; o += up((size_t)c->max_seqs * (2 + c->k_max) * 4);
   // staging block: one host->device copy per call
   size_t so = 0;
   L.s_tok = so; so += L.Rmax * 4;
@@ -231,6 +233,7 @@ void bind_work(ee_ctx* c) {
   w.ptable = reinterpret_cast<int*>(sb + L.s_ptable);
   w.info = reinterpret_cast<int*>(sb + L.s_info);
   w.ptable_len = L.ptable_len;
+  w.rec = 2 + c->cfg.k_max;
   w.max_splits = L.max_splits;
 }
 
@@ -305,7 +308,7 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
 // Stage the per-sequence state (page tables, committed lengths, the KV slot
 // of every row), run the forward + acceptance (+ tree compaction) of B
 // sequences of T rows whose tokens, positions and parents the caller staged,
-// and fetch the results (record b at h_result + b * (2 + 64)).  Mode 3 uses
+// and fetch the results (record b at h_result + b * (2 + k_max)).  Mode 3 uses
 // the top-k size and dynamic flag given for every sequence.
 int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0, int dynamic = 0) {
   const Layout& L = c->lay;
@@ -338,7 +341,7 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
     c->prof.used = 0;
     HIP_TRY(c, launch_block(c, step, prof));
   }
-  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (size_t)B * (2 + 64) * sizeof(int),
+  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (size_t)B * c->w.rec * sizeof(int),
                             hipMemcpyDeviceToHost, c->st));
   HIP_TRY(c, hipStreamSynchronize(c->st));
   for (int i = 0; prof && i < c->prof.used; ++i) {
@@ -406,7 +409,8 @@ int verify_many(ee_ctx* c, int n_seq, const int32_t* seqs, const int32_t* drafts
     return fail(c, EE_EINVAL, "seqs, accept_lens and next_tokens must be non-NULL");
   if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
   const int T = K + 1;
-  std::vector<int> depth((size_t)n_seq * 65);
+  if (parents && K > MAX_TREE) return fail(c, EE_EINVAL, "draft trees have at most 64 nodes");
+  std::vector<int> depth((size_t)n_seq * (MAX_TREE + 1));
   std::vector<Seq*> ss(n_seq);
   for (int b = 0; b < n_seq; ++b) {
     int rc = check_seq(c, seqs[b]);
@@ -417,7 +421,7 @@ int verify_many(ee_ctx* c, int n_seq, const int32_t* seqs, const int32_t* drafts
     if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
     if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
     if ((rc = check_draft(c, drafts ? drafts + (size_t)b * K : nullptr, K,
-                          parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65])))
+                          parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * (MAX_TREE + 1)])))
       return rc;
     ss[b] = &s;
   }
@@ -430,7 +434,7 @@ int verify_many(ee_ctx* c, int n_seq, const int32_t* seqs, const int32_t* drafts
   }
   for (int b = 0; b < n_seq; ++b)
     stage_draft(c, b, T, *ss[b], drafts ? drafts + (size_t)b * K : nullptr,
-                parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * 65]);
+                parents ? parents + (size_t)b * K : nullptr, &depth[(size_t)b * (MAX_TREE + 1)]);
   const int mode = top_k ? 3 : (parents ? 2 : 1);
   const int rc = run_block(c, ss.data(), n_seq, T, mode, top_k, dynamic);
   if (rc) {
@@ -438,7 +442,7 @@ int verify_many(ee_ctx* c, int n_seq, const int32_t* seqs, const int32_t* drafts
     return rc;
   }
   for (int b = 0; b < n_seq; ++b) {
-    const int* res = c->h_result + (size_t)b * (2 + 64);
+    const int* res = c->h_result + (size_t)b * c->w.rec;
     const int a = res[0];
     ss[b]->len += 1 + a;
     ss[b]->pending = res[1];
@@ -512,7 +516,7 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
   };
   hipError_t e;
   if ((e = hipHostMalloc(reinterpret_cast<void**>(&c->h_stage), L.stage_bytes, hipHostMallocDefault)) != hipSuccess ||
-      (e = hipHostMalloc(reinterpret_cast<void**>(&c->h_result), (size_t)cfg->max_seqs * (2 + 64) * sizeof(int),
+      (e = hipHostMalloc(reinterpret_cast<void**>(&c->h_result), (size_t)cfg->max_seqs * (2 + cfg->k_max) * sizeof(int),
                           hipHostMallocDefault)) != hipSuccess) {
     hip_fail(c, e, "hipHostMalloc");
     return cleanup(EE_EHIP);
@@ -649,7 +653,8 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   Seq& s = c->seqs[seq];
   if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
   if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
-  int depth[65];
+  if (parent && K > MAX_TREE) return fail(c, EE_EINVAL, "draft trees have at most 64 nodes");
+  int depth[MAX_TREE + 1];
   if ((rc = check_draft(c, draft, K, parent, depth))) return rc;
   const int T = K + 1;
   if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");

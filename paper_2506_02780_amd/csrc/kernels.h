@@ -70,18 +70,19 @@ struct Work {
   unsigned long long* amax; // [Rmax, ceil(V/2048), 8] chunk maxima (top-8 in mode 3)
   int* greedy;              // [Rmax]
   int* verdict;             // [Rmax] mode 3: tau | draft-accepted << 8
-  int* result;              // [max_seqs][2 + 64]: accept_len, next, accepted rows
+  int* result;              // [max_seqs][rec]: accept_len, next, accepted rows (or thresholds)
   // staged per call (host -> device)
   int* tok;                 // [Rmax]
   int* pos;                 // [Rmax] rotary position of each row
   int* prow;                // [Rmax] parent row within the sequence (tree) or t-1
   int* slot;                // [Rmax] KV-pool slot (page * 64 + offset) the row's K/V go to
-  unsigned char* path;      // [Rmax][64] tree mode: entry j-1 of row t = block row at
-                            // depth j on t's path (row 0, the pending token, is depth 0)
+  unsigned char* path;      // [Rmax][64] tree mode (at most 64 nodes): entry j-1 of row t =
+                            // block row at depth j on t's path (row 0, the pending token, is depth 0)
   int* ptable;              // [max_seqs][ptable_len] page of each 64-position block
   int* info;                // [max_seqs][4]: committed positions n, attention splits in use,
                             // top-k size k and dynamic flag (mode 3)
   int ptable_len;           // entries per sequence (multiple of 4)
+  int rec;                  // ints per result record: 2 + k_max
   int max_splits;           // attention splits of the longest context
 };
 

@@ -1,7 +1,7 @@
 // gfx950 kernels of the greedy speculative-verification step.
 //
-// One verify step runs the target model over a block of T <= 65 rows (the
-// pending token plus up to 64 draft tokens, Eq. 3), decodes every row
+// One verify step runs the target model over a block of T <= 513 rows (the
+// pending token plus up to 512 draft tokens, Eq. 3), decodes every row
 // greedily and accepts the longest matching draft prefix (Eq. 7).  Weight
 // streaming dominates: every linear layer is a skinny GEMM with T rows, so
 // each weight byte is read once per step and the GEMMs are HBM-bound.
@@ -1254,12 +1254,13 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
                                                     const int* __restrict__ prow,
                                                     const int* __restrict__ greedy,
                                                     const int* __restrict__ verdict, int T, int mode,
-                                                    int* __restrict__ result) {
-  // workgroup b: sequence b, rows b*T .. b*T + T - 1, result record b
+                                                    int* __restrict__ result, int rec) {
+  // workgroup b: sequence b, rows b*T .. b*T + T - 1, result record b (rec ints)
   tok += blockIdx.x * T;
   prow += blockIdx.x * T;
   greedy += blockIdx.x * T;
-  result += blockIdx.x * (2 + 64);
+  verdict += blockIdx.x * T;
+  result += blockIdx.x * rec;
   const int lane = threadIdx.x;
   const int K = T - 1;
   if (mode == 0) {
@@ -1269,32 +1270,36 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
     }
     return;
   }
-  if (mode == 3) {
-    // draft d_{i+1} passes when row i's verdict accepted it; result[2+i] = tau of row i
-    verdict += blockIdx.x * T;
-    const int vd = lane < K ? verdict[lane] : 0;
-    const unsigned long long b = __ballot(lane < K && !((vd >> 8) & 1));
-    const int a = b ? __ffsll((long long)b) - 1 : K;
+  if (mode == 1 || mode == 3) {
+    // draft d_{i+1} (row i+1) is checked against row i: its greedy token
+    // (mode 1) or its top-k verdict (mode 3); the first failing row, found 64
+    // rows at a time, is a.  Mode 3 also records every row's threshold.
+    int a = K;
+    for (int i0 = 0; i0 < K; i0 += 64) {
+      const int i = i0 + lane;
+      bool fails = false;
+      if (i < K) {
+        if (mode == 1) {
+          fails = tok[i + 1] != greedy[i];
+        } else {
+          const int vd = verdict[i];
+          fails = !((vd >> 8) & 1);
+          result[2 + i] = vd & 0xff;
+        }
+      }
+      const unsigned long long b = __ballot(fails);
+      if (b && a == K) a = i0 + __ffsll((long long)b) - 1;
+      if (mode == 1 && a != K) break;
+    }
     if (lane == 0) {
       result[0] = a;
       result[1] = greedy[a];
     }
-    if (lane < K) result[2 + lane] = vd & 0xff;
+    if (mode == 1)
+      for (int i = lane; i < a; i += 64) result[2 + i] = i + 1;
     return;
   }
-  if (mode == 1) {
-    // draft d_{i+1} (row i+1) is checked against the greedy token of row i
-    const bool mism = lane < K && tok[lane + 1] != greedy[lane];
-    const unsigned long long b = __ballot(mism);
-    const int a = b ? __ffsll((long long)b) - 1 : K;
-    if (lane == 0) {
-      result[0] = a;
-      result[1] = greedy[a];
-    }
-    if (lane < a) result[2 + lane] = lane + 1;
-    return;
-  }
-  // tree walk from row 0
+  // tree walk from row 0 (trees have at most 64 nodes)
   int cur = 0, a = 0;
   for (;;) {
     const bool hit = lane < K && prow[lane + 1] == cur && tok[lane + 1] == greedy[cur];
@@ -1317,11 +1322,11 @@ __global__ __launch_bounds__(256) void compact_kernel(void* __restrict__ kv_pool
                                                       const int* __restrict__ ptable,
                                                       const int* __restrict__ result,
                                                       const int* __restrict__ info, int Hkv,
-                                                      int ptable_len) {
+                                                      int ptable_len, int rec) {
   constexpr int ESZ = Geo<DT>::ESZ;
   // blockIdx.y: sequence
   ptable += blockIdx.y * ptable_len;
-  result += blockIdx.y * (2 + 64);
+  result += blockIdx.y * rec;
   const int n = info[4 * blockIdx.y];
   const int layer = blockIdx.x / Hkv, g = blockIdx.x % Hkv;
   const int a = result[0];
@@ -1501,7 +1506,7 @@ hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, 
   (void)m;
   return timed(prof, PC_ACCEPT, st, [&] {
     hipLaunchKernelGGL(accept_kernel, dim3(s.B), dim3(64), 0, st, w.tok, w.prow, w.greedy, w.verdict, s.T,
-                       s.mode, w.result);
+                       s.mode, w.result, w.rec);
     return hipGetLastError();
   });
 }
@@ -1511,11 +1516,11 @@ hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof,
   const dim3 grid(m.L * m.Hkv, s.B), block(256);
   return timed(prof, PC_COMPACT, st, [&] {
     if (m.dt == DT_BF16 && m.hd == 128)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 128>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len, w.rec);
     else if (m.dt == DT_BF16 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
+      hipLaunchKernelGGL((compact_kernel<DT_BF16, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len, w.rec);
     else if (m.dt == DT_F32 && m.hd == 64)
-      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len);
+      hipLaunchKernelGGL((compact_kernel<DT_F32, 64>), grid, block, 0, st, m.kv_pool, layer_elems, w.ptable, w.result, w.info, m.Hkv, w.ptable_len, w.rec);
     else
       return hipErrorInvalidValue;   // fp32 with head_dim 128 would exceed the LDS staging size
     return hipGetLastError();
