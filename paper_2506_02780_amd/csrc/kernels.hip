@@ -25,6 +25,8 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include <algorithm>
+
 namespace ee {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -171,10 +173,12 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned off) {
 
 struct GemmArgs {
   const uint4* w;       // packed weights [n_tiles][S][64]
-  const uint4* x;       // packed activations of this launch's rows [MT][S][64]
-  float* part;          // [SK][Ttot][N]; this launch writes rows row0 .. row0 + T - 1
-  int S, SK, SS, T, N, n_tiles;
-  int row0, Ttot;
+  const uint4* x;       // packed activations of all Ttot rows [ceil(Ttot/16)][S][64]
+  float* part;          // [SK][Ttot][N]
+  int S, SK, SS, N, n_tiles;
+  int Ttot;             // rows of the block
+  int rows;             // rows per row group (a multiple of 16, at most 16 MT)
+  int P, G;             // workgroups per row group (G tile groups x SK slices used), tile groups
 };
 
 inline int gemm_slices(int S) {
@@ -183,30 +187,42 @@ inline int gemm_slices(int S) {
   return sk;   // <= 16 for every K the library accepts (K <= 32768)
 }
 
-template <int DT, int MT>
+// Workgroup (row group rg, tile group g, slice k) = blockIdx rg * P + g * SK + k
+// holds the activation fragments of its rows for slice k in registers and
+// streams the weight tiles g, g + G, ...  Every row group repeats the same
+// weight stream; with P a multiple of 8 the workgroups that share a stream
+// sit on the same XCD (workgroups are dealt to the 8 XCDs in turn) and run
+// side by side, so one of them fetches each weight tile from HBM and the
+// others find it in that XCD's L2.  NT: non-temporal weight loads (one row
+// group: nothing re-reads them).
+template <int DT, int MT, bool NT>
 __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, c = lane & 15;
-  const int k = blockIdx.x % a.SK, groups = gridDim.x / a.SK;
+  const int rg = blockIdx.x / a.P, q = blockIdx.x - rg * a.P;
+  if (q >= a.SK * a.G) return;
+  const int k = q % a.SK, groups = a.G;
+  const int row0 = rg * a.rows, T = min(a.rows, a.Ttot - row0);
   const int S = a.S, s0 = k * a.SS, ns = min(S - s0, a.SS);
-  const auto xs = make_rsrc(a.x, (unsigned)(MT * S * 1024));
+  const auto xs = make_rsrc(a.x + (size_t)(row0 / 16) * S * 64, (unsigned)(MT * S * 1024));
   const auto ws = make_rsrc(a.w, (unsigned)((size_t)a.n_tiles * S * 1024));
+  constexpr int WAUX = NT ? 2 : 0;
   uint4 xr[GEMM_SPW][MT];
 #pragma unroll
   for (int i = 0; i < GEMM_SPW; ++i) {
     const int sl = wv + GEMM_WAVES * i;
 #pragma unroll
     for (int m = 0; m < MT; ++m)
-      xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < a.T)
+      xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < T)
                                   ? (unsigned)(((m * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
   __shared__ f32x4 red[2][GEMM_WAVES][MT][64];
   uint4 wr[GEMM_SPW];
-  int tile = blockIdx.x / a.SK;
+  int tile = q / a.SK;
 #pragma unroll
   for (int i = 0; i < GEMM_SPW; ++i) {
     const int sl = wv + GEMM_WAVES * i;
-    wr[i] = bload<2>(ws, (tile < a.n_tiles && sl < ns)
-                             ? (unsigned)(((tile * S + s0 + sl) * 64 + lane) * 16) : OOB);
+    wr[i] = bload<WAUX>(ws, (tile < a.n_tiles && sl < ns)
+                                ? (unsigned)(((tile * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
   for (int it = 0; tile < a.n_tiles; tile += groups, ++it) {
     const int tn = tile + groups;
@@ -217,8 +233,8 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
     for (int i = 0; i < GEMM_SPW; ++i) {
       const uint4 wf = wr[i];
       const int sl = wv + GEMM_WAVES * i;
-      wr[i] = bload<2>(ws, (tn < a.n_tiles && sl < ns)
-                               ? (unsigned)(((tn * S + s0 + sl) * 64 + lane) * 16) : OOB);
+      wr[i] = bload<WAUX>(ws, (tn < a.n_tiles && sl < ns)
+                                  ? (unsigned)(((tn * S + s0 + sl) * 64 + lane) * 16) : OOB);
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[m] = mma<DT>(wf, xr[i][m], acc[m]);
     }
@@ -226,54 +242,57 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) red[pb][wv][m][lane] = acc[m];
     __syncthreads();
-    for (int q = threadIdx.x; q < MT * 64; q += GEMM_WAVES * 64) {
-      const int m = q >> 6, ln = q & 63;
+    for (int qq = threadIdx.x; qq < MT * 64; qq += GEMM_WAVES * 64) {
+      const int m = qq >> 6, ln = qq & 63;
       f32x4 v = red[pb][0][m][ln];
 #pragma unroll
       for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][m][ln];
       const int t = m * 16 + (ln & 15);
-      if (t < a.T) {
-        float* o = a.part + ((size_t)k * a.Ttot + a.row0 + t) * a.N + tile * 16 + 4 * (ln >> 4);
+      if (t < T) {
+        float* o = a.part + ((size_t)k * a.Ttot + row0 + t) * a.N + tile * 16 + 4 * (ln >> 4);
         *reinterpret_cast<float4*>(o) = make_float4(v.x, v.y, v.z, v.w);
       }
     }
   }
 }
 
-constexpr int GEMM_MAX_ROWS = 80;   // rows one launch holds in registers (MT <= 5)
+constexpr int GEMM_MAX_ROWS = 80;   // rows one workgroup holds in registers (MT <= 5)
 
-// Y = X W^T for R rows: launches of at most GEMM_MAX_ROWS rows each (every
-// launch streams the weights once; a row's arithmetic is the same in any
-// launch).
+// Y = X W^T for R rows.  Up to 80 rows: one row group, one workgroup per CU,
+// each streaming its weight tiles once.  More rows: groups of 80 rows in
+// the same launch, sharing each weight stream through L2.  A row's
+// arithmetic is the same either way (and the same as in a launch of its own).
 template <int DT>
 static hipError_t gemm(const uint4* w, const uint4* x, int N, int K, int R, float* part,
                        hipStream_t st) {
   GemmArgs a;
-  a.w = w; a.part = part; a.N = N; a.Ttot = R;
+  a.w = w; a.x = x; a.part = part; a.N = N; a.Ttot = R;
   a.S = K / Geo<DT>::KS;
   a.SK = gemm_slices(a.S);
   a.SS = (a.S + a.SK - 1) / a.SK;
   a.n_tiles = N / 16;
-  int groups = 256 / a.SK;
-  if (groups < 1) groups = 1;
-  if (groups > a.n_tiles) groups = a.n_tiles;
-  const dim3 grid(groups * a.SK), block(GEMM_WAVES * 64);
-  for (int r0 = 0; r0 < R; r0 += GEMM_MAX_ROWS) {
-    a.row0 = r0;
-    a.T = R - r0 < GEMM_MAX_ROWS ? R - r0 : GEMM_MAX_ROWS;
-    a.x = x + (size_t)(r0 / 16) * a.S * 64;   // r0 is a multiple of 16
-    switch ((a.T + 15) / 16) {
-      case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1>), grid, block, 0, st, a); break;
-      case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2>), grid, block, 0, st, a); break;
-      case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3>), grid, block, 0, st, a); break;
-      case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4>), grid, block, 0, st, a); break;
-      case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5>), grid, block, 0, st, a); break;
+  const dim3 block(GEMM_WAVES * 64);
+  if (R <= GEMM_MAX_ROWS) {
+    a.rows = R;
+    a.G = std::max(1, std::min(256 / a.SK, a.n_tiles));
+    a.P = a.G * a.SK;
+    const dim3 grid(a.P);
+    switch ((R + 15) / 16) {
+      case 1: hipLaunchKernelGGL((gemm_kernel<DT, 1, true>), grid, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((gemm_kernel<DT, 2, true>), grid, block, 0, st, a); break;
+      case 3: hipLaunchKernelGGL((gemm_kernel<DT, 3, true>), grid, block, 0, st, a); break;
+      case 4: hipLaunchKernelGGL((gemm_kernel<DT, 4, true>), grid, block, 0, st, a); break;
+      case 5: hipLaunchKernelGGL((gemm_kernel<DT, 5, true>), grid, block, 0, st, a); break;
       default: return hipErrorInvalidValue;
     }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    return hipGetLastError();
   }
-  return hipSuccess;
+  a.rows = GEMM_MAX_ROWS;
+  const int rg = (R + GEMM_MAX_ROWS - 1) / GEMM_MAX_ROWS;
+  a.P = std::max(256 / rg / 8 * 8, (a.SK + 7) / 8 * 8);
+  a.G = std::max(1, std::min(a.P / a.SK, a.n_tiles));
+  hipLaunchKernelGGL((gemm_kernel<DT, 5, false>), dim3(rg * a.P), block, 0, st, a);
+  return hipGetLastError();
 }
 
 constexpr int MAX_SLICES = 16;   // gemm_slices() never exceeds this for K <= 32768
