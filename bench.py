@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
+LONG_K = 512                      # longest draft the engine is built for
 # The Reuse driver resumes at a match of at least this many generated tokens;
 # shorter (single-token) matches are frequent by chance and can move the
 # cursor past the true position in the original code.
@@ -224,6 +225,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
     ap.add_argument("--no-33b", action="store_true", help="skip the 33B batch-of-4 measurement")
+    ap.add_argument("--no-long", action="store_true", help="skip the long-draft (K = 128..512) measurement")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -243,8 +245,8 @@ def main():
     t0 = time.perf_counter()
     weights = gen_weights(shape, seed=1234)
     log(f"[bench] weights drawn in {time.perf_counter() - t0:.1f}s")
-    max_ctx = ctx + args.gen + 66
-    eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=64)
+    max_ctx = max(ctx + args.gen + 66, ctx + LONG_K + 2)
+    eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=LONG_K)
     if args.eager:
         eng.use_graphs(False)
     log(f"[bench] engine ready at {time.perf_counter() - t0:.1f}s")
@@ -252,8 +254,10 @@ def main():
     prompt = zipf_tokens(shape.vocab, ctx, seed=42)
     first = eng.prefill(0, prompt)
     G = [first]
-    for _ in range(args.gen - 1):
+    for _ in range((args.gen if args.no_long else max(args.gen, LONG_K + 1)) - 1):
         G.append(eng.verify(0, [])[1])
+    G_long = list(G)             # the continuation long drafts are taken from
+    G = G[:args.gen]
     code, _ = inject_edits(np.asarray(G, dtype=np.int32), shape.vocab, seed=7)
     code = code.tolist()
     log(f"[bench] prompt + {args.gen}-token greedy output ready at {time.perf_counter() - t0:.1f}s")
@@ -339,6 +343,16 @@ def main():
     ttoks = tree_tokens(parent, G[1:9], shape.vocab, seed=11)
     l50, l90, acc = fixed_ctx(ttoks, parent)
     tree64 = dict(lat_entry(64, l50, l90, acc), nodes=64, max_depth=8, max_branch=3)
+
+    # long Reuse drafts: one block of K + 1 rows verifies a long span (the
+    # model's own continuation, so every draft token is accepted)
+    long_drafts = {}
+    for kk in (() if args.no_long else (128, 256, LONG_K)):
+        l50, l90, acc = fixed_ctx(list(G_long[1:1 + kk]), reps=30)
+        e = lat_entry(kk, l50, l90, acc)
+        fl = 2 * (kk + 1) * linear_weight_bytes(shape) // 2 + attention_flops(shape, kk + 1, ctx)
+        e["mfma_frac"] = round(fl / l50 / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+        long_drafts[str(kk)] = e
 
     # entropy-aware dynamic and fixed top-k verification (Eq. 9-10) on the
     # same draft as the headline latency, with the per-class time of the
@@ -429,6 +443,7 @@ def main():
         "breakdown_ms_per_step": brk,
         "k_sweep_at_ctx": k_sweep,
         "tree64_at_ctx": tree64,
+        "long_drafts_at_ctx": long_drafts or None,
         "entropy_verify_at_ctx": entropy,
         "lossless_check": "emitted stream equals the GPU's own greedy output",
     }
