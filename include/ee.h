@@ -103,6 +103,17 @@ int32_t ee_destroy(ee_ctx* ctx);
 int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
                    int32_t* next_token);
 
+/* Append tokens[0..n-1] to sequence `seq` without verification (n >= 0): the
+ * block [pending, tokens...] is run in blocks of at most k_max+1 rows and all
+ * n+1 positions are committed; *next_token = the greedy token of the last row,
+ * which becomes pending.  For a model that must follow tokens chosen
+ * elsewhere (a draft model catching up with the accepted output); n = 0 is
+ * one greedy decoding step.  Errors: EE_ESTATE before prefill; EE_EINVAL for
+ * a token outside [0, vocab); EE_ECAPACITY if len + n + 2 would exceed
+ * max_ctx or the KV pool has no free page (nothing is committed then). */
+int32_t ee_extend(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
+                  int32_t* next_token);
+
 /* One verification step (Eq. 3 forward + Eq. 7 acceptance).  The block is
  * [pending, d_1..d_K]: row 0 is the pending token at position len; draft row
  * i sits at position len + depth(i).  Every row is decoded greedily (argmax
@@ -182,6 +193,68 @@ int32_t ee_seq_state(ee_ctx* ctx, int32_t seq, int32_t* len, int32_t* pending_to
 int32_t ee_match_reuse(const int32_t* generated, int32_t n_gen, const int32_t* original,
                        int32_t n_orig, int32_t cursor, int32_t min_ngram, int32_t max_ngram,
                        int32_t* draft_start, int32_t* match_len);
+
+/* Edit-session driver: the Reuse and Generate phases (Sec. "Reuse",
+ * Sec. "Generate") over a target-model sequence and, optionally, a
+ * draft-model sequence in another context (a smaller model on the same GPU).
+ * Both sequences must hold the same prompt; ee_edit_begin makes the draft
+ * sequence's pending token the target's (the first emitted token).
+ *
+ * One ee_edit_step runs one step of the current phase and appends the tokens
+ * it emits to the caller's output buffer:
+ *   Reuse: the matcher (ee_match_reuse with min_match, max_match; while the
+ *     output is shorter than min_match, the whole output) looks for the
+ *     output's suffix in the original code from the cursor on; the draft
+ *     is the next k_reuse original tokens after the match, or after the cursor
+ *     when nothing matches.  Greedy verification (Eq. 7); cursor := draft
+ *     start + accepted + 1 (the rejected token is taken as substituted).  A
+ *     rejection marks an edit position: the next step is Generate.  A step
+ *     whose draft would be empty (the original is used up) runs as Generate.
+ *   Generate: the draft model catches up with the output (ee_extend), drafts
+ *     gamma tokens greedily, and the target verifies them with Eq. 7
+ *     (top_k = 0) or Eq. 9-10 (top_k >= 1, `dynamic` as in ee_verify_topk);
+ *     the draft sequence is rolled back to the accepted prefix.  Without a
+ *     draft context (draft == NULL) the step is one plain greedy step.  After
+ *     the step the matcher is run; a match switches back to Reuse.
+ * out[0..n_out-1] is the session output so far (the first call passes the
+ * first emitted token, n_out = 1); out[n_out-1] must be the target's pending
+ * token.  The new tokens (accepted draft tokens, then the target's next
+ * token) are written at out[n_out..n_out+*n_new-1]; out_cap >= n_out +
+ * max(k_reuse, gamma) + 1.  With top_k = 0 the output is exactly the target's
+ * greedy decoding whatever the draft model proposes.
+ * Errors: EE_EINVAL for bad parameters; EE_ESTATE if out does not end with
+ * the target's pending token or the draft sequence does not follow the
+ * output; capacity and HIP errors as the calls it makes.  On an error the
+ * target sequence is unchanged; the draft sequence is realigned by the next
+ * call. */
+enum { EE_PHASE_REUSE = 0, EE_PHASE_GENERATE = 1 };
+
+typedef struct {
+  int32_t k_reuse;      /* draft tokens per Reuse step, 1..k_max of the target   */
+  int32_t gamma;        /* draft-model tokens per Generate step, 1..k_max         */
+  int32_t top_k;        /* Generate verification: 0 greedy, 1..8 Eq. 9-10         */
+  int32_t dynamic;      /* with top_k: entropy-aware tau (1) or fixed top-k (0)   */
+  int32_t min_match;    /* shortest output suffix whose match resumes Reuse (>=1) */
+  int32_t max_match;    /* longest suffix tried (>= min_match)                    */
+} ee_edit_params;
+
+typedef struct {
+  int32_t phase;          /* phase of the next step                                */
+  int32_t cursor;         /* original position a Reuse draft falls back to         */
+  int32_t last_phase;     /* phase of the last step                                */
+  int32_t last_accept;    /* draft tokens accepted by the last step                */
+  int64_t steps[2];       /* steps run per phase                                   */
+  int64_t emitted[2];     /* tokens emitted per phase                              */
+  int64_t draft_tokens;   /* tokens proposed by the draft model                    */
+  int64_t draft_forwards; /* forward blocks run by the draft model                 */
+} ee_edit_state;
+
+int32_t ee_edit_begin(ee_ctx* target, int32_t seq, ee_ctx* draft, int32_t draft_seq,
+                      ee_edit_state* state);
+int32_t ee_edit_step(ee_ctx* target, int32_t seq, ee_ctx* draft, int32_t draft_seq,
+                     const int32_t* original, int32_t n_orig, const ee_edit_params* params,
+                     ee_edit_state* state, int32_t* out, int32_t n_out, int32_t out_cap,
+                     int32_t* n_new);
 
 /* Copy the logits of the last prefill block or verify block (rows x vocab,
  * fp32, row-major) to host memory; rows must equal that block's row count.

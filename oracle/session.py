@@ -9,6 +9,8 @@ Conventions (the paper leaves them open):
   pointers), accepts by Eq. 7 / the tree walk, commits the pending row plus
   the accepted rows in depth order (n -> n + 1 + a) and makes the emitted
   next token pending.  K = 0 is one plain greedy step of Eq. 1.
+* ``extend`` commits [pending, tokens...] without verification (a draft
+  model catching up with the accepted output).
 * ``verify_topk`` is ``verify`` of a chain with the entropy-aware (or fixed)
   top-k acceptance of Eq. 9-10 in place of Eq. 7; ``score`` returns the
   logits of a chain block without committing anything.
@@ -77,6 +79,18 @@ class OracleSession:
         self.pending = nxt
         self.last_logits = logits
         return a, nxt, path
+
+    def extend(self, tokens):
+        """Commit [pending, tokens...] without verification (a model following
+        tokens chosen elsewhere); the greedy token after the last becomes
+        pending and is returned."""
+        rows = np.concatenate([[self.pending], np.asarray(tokens, dtype=np.int64)])
+        depth, vis = chain_structure(len(rows))
+        logits, blk = forward_block(self.shape, self.weights, self.cache, rows, depth, vis)
+        self._commit(blk, np.arange(len(rows)))
+        self.pending = int(greedy_rows(logits[-1:])[0])
+        self.last_logits = logits
+        return self.pending
 
     def score(self, draft):
         """Logits of the chain [pending, d_1..d_K]; the cache is unchanged."""

@@ -61,6 +61,7 @@ ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_batch = _sig("ee_verify_batch", _i32, [_vp, _i32, _pi32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_topk = _sig("ee_verify_topk", _i32, [_vp, _i32, _pi32, _pi32, _i32, _i32, _i32, _pi32, _pi32, _pi32])
+ee_extend = _sig("ee_extend", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_kv_rollback = _sig("ee_kv_rollback", _i32, [_vp, _i32, _i32, _i32])
 ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
 ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32, _i32, _i32, _pi32, _pi32])
@@ -74,6 +75,25 @@ ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_do
 
 PROF_CLASSES = ("norm", "qkv", "attn", "combine", "oproj", "gateup", "down", "lmhead", "argmax",
                 "accept", "compact", "finish")
+
+
+EE_PHASE_REUSE, EE_PHASE_GENERATE = 0, 1
+
+
+class EEEditParams(ctypes.Structure):
+    _fields_ = [("k_reuse", _i32), ("gamma", _i32), ("top_k", _i32), ("dynamic", _i32),
+                ("min_match", _i32), ("max_match", _i32)]
+
+
+class EEEditState(ctypes.Structure):
+    _fields_ = [("phase", _i32), ("cursor", _i32), ("last_phase", _i32), ("last_accept", _i32),
+                ("steps", ctypes.c_int64 * 2), ("emitted", ctypes.c_int64 * 2),
+                ("draft_tokens", ctypes.c_int64), ("draft_forwards", ctypes.c_int64)]
+
+
+ee_edit_begin = _sig("ee_edit_begin", _i32, [_vp, _i32, _vp, _i32, ctypes.POINTER(EEEditState)])
+ee_edit_step = _sig("ee_edit_step", _i32, [_vp, _i32, _vp, _i32, _pi32, _i32, ctypes.POINTER(EEEditParams),
+                                           ctypes.POINTER(EEEditState), _pi32, _i32, _i32, _pi32])
 
 
 class EEError(RuntimeError):
@@ -173,6 +193,15 @@ class Engine:
         _check(ee_prefill(self.ctx, seq, tp, len(t), ctypes.byref(nxt)), self.ctx)
         self._last_rows = min(len(t) - (len(t) - 1) // (self.cfg.k_max + 1) * (self.cfg.k_max + 1),
                               self.cfg.k_max + 1)
+        return nxt.value
+
+    def extend(self, seq: int, tokens) -> int:
+        """Commit [pending, tokens...] without verification; returns the new
+        pending token (the greedy token after the last one)."""
+        t, tp = _i32arr(tokens)
+        nxt = ctypes.c_int32()
+        _check(ee_extend(self.ctx, seq, tp if len(t) else None, len(t), ctypes.byref(nxt)), self.ctx)
+        self._last_rows = (len(t) + 1) - len(t) // (self.cfg.k_max + 1) * (self.cfg.k_max + 1)
         return nxt.value
 
     def verify(self, seq: int, draft, parent=None):
@@ -292,3 +321,37 @@ class Engine:
             self.close()
         except Exception:
             pass
+
+
+class EditSession:
+    """An edit session over a target engine's sequence and, optionally, a
+    draft engine's sequence holding the same prompt (ee_edit_begin /
+    ee_edit_step).  ``output`` is the emitted token stream so far."""
+
+    def __init__(self, target: Engine, seq: int, original, draft: Engine | None = None, draft_seq: int = 0,
+                 k_reuse: int = 32, gamma: int = 7, top_k: int = 0, dynamic: bool = True,
+                 min_match: int = 3, max_match: int = 8, capacity: int = 1 << 16):
+        self.target, self.seq, self.draft, self.draft_seq = target, seq, draft, draft_seq
+        self.original, self._op = _i32arr(original)
+        self.params = EEEditParams(k_reuse, gamma, top_k, int(bool(dynamic)), min_match, max_match)
+        self.state = EEEditState()
+        _check(ee_edit_begin(target.ctx, seq, draft.ctx if draft else None, draft_seq,
+                             ctypes.byref(self.state)), target.ctx)
+        self._out = np.zeros(capacity, dtype=np.int32)
+        self._out[0] = target.seq_state(seq)[1]
+        self.n = 1
+
+    @property
+    def output(self):
+        return self._out[:self.n].tolist()
+
+    def step(self):
+        """One Reuse or Generate step; returns (phase, new tokens)."""
+        nn = ctypes.c_int32()
+        _check(ee_edit_step(self.target.ctx, self.seq, self.draft.ctx if self.draft else None, self.draft_seq,
+                            self._op, len(self.original), ctypes.byref(self.params), ctypes.byref(self.state),
+                            self._out.ctypes.data_as(_pi32), self.n, len(self._out), ctypes.byref(nn)),
+               self.target.ctx)
+        new = self._out[self.n:self.n + nn.value].tolist()
+        self.n += nn.value
+        return self.state.last_phase, new

@@ -396,6 +396,37 @@ void stage_draft(ee_ctx* c, int b, int T, const Seq& s, const int32_t* draft, co
   }
 }
 
+// Run rows[0..n) at positions len.. in blocks of at most k_max + 1 rows and
+// commit all of them (every row's K/V kept); *last = the greedy token of the
+// final row.  On failure the sequence is left as it was.
+int commit_rows(ee_ctx* c, Seq& s, const int32_t* rows, int n, int* last) {
+  const Layout& L = c->lay;
+  int added;
+  if (!reserve_pages(c, s, s.len + n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
+  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
+  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
+  const int len0 = s.len;
+  for (int off = 0; off < n; off += L.Tmax) {
+    const int T = std::min(L.Tmax, n - off);
+    for (int r = 0; r < T; ++r) {
+      tok[r] = rows[off + r];
+      pos[r] = s.len + r;
+      prow[r] = r - 1;
+    }
+    Seq* one = &s;
+    const int rc = run_block(c, &one, 1, T, 0);
+    if (rc) {
+      s.len = len0;
+      unreserve(c, s, added);
+      return rc;
+    }
+    s.len += T;
+    *last = c->h_result[1];
+  }
+  return EE_OK;
+}
+
 // One block of n_seq sequences with K draft tokens each: greedy (top_k 0;
 // linear, or trees when `parents` is given) or top-k verification (top_k >= 1,
 // linear).  Everything is validated and every page reserved before anything
@@ -614,32 +645,29 @@ int32_t ee_prefill(ee_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, int
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "token outside [0, vocab)");
   if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "prompt longer than max_ctx - 1");
-  int added;
-  if (!reserve_pages(c, s, n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
-  const Layout& L = c->lay;
-  int* tok = reinterpret_cast<int*>(c->h_stage + L.s_tok);
-  int* pos = reinterpret_cast<int*>(c->h_stage + L.s_pos);
-  int* prow = reinterpret_cast<int*>(c->h_stage + L.s_prow);
-  const int len0 = s.len;
-  int last = -1;
-  for (int off = 0; off < n; off += L.Tmax) {
-    const int T = std::min(L.Tmax, n - off);
-    for (int r = 0; r < T; ++r) {
-      tok[r] = tokens[off + r];
-      pos[r] = s.len + r;
-      prow[r] = r - 1;
-    }
-    Seq* one = &s;
-    rc = run_block(c, &one, 1, T, 0);
-    if (rc) {   // leave the sequence empty, as before the call
-      s.len = len0;
-      unreserve(c, s, added);
-      return rc;
-    }
-    s.len += T;
-    last = c->h_result[1];
-  }
+  int last;
+  if ((rc = commit_rows(c, s, tokens, n, &last))) return rc;
   s.live = true;
+  s.pending = last;
+  *next_token = last;
+  return EE_OK;
+}
+
+int32_t ee_extend(ee_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, int32_t* next_token) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if ((n > 0 && !tokens) || !next_token) return fail(c, EE_EINVAL, "tokens and next_token must be non-NULL");
+  if (n < 0) return fail(c, EE_EINVAL, "n must be >= 0");
+  Seq& s = c->seqs[seq];
+  if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "extend before prefill");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "token outside [0, vocab)");
+  if ((size_t)s.len + n + 2 > (size_t)c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "sequence would exceed max_ctx");
+  std::vector<int32_t> rows((size_t)n + 1);
+  rows[0] = s.pending;
+  for (int i = 0; i < n; ++i) rows[i + 1] = tokens[i];
+  int last;
+  if ((rc = commit_rows(c, s, rows.data(), n + 1, &last))) return rc;
   s.pending = last;
   *next_token = last;
   return EE_OK;
