@@ -206,6 +206,66 @@ def batch_config(ee, name: str, n_seq: int, k: int, ctx: int, reps: int = 20) ->
             "emitted_tokens_per_s": round(n_seq * (k + 1) / p50, 1), "setup_s": round(setup_s, 1)}
 
 
+def edit_sessions(ee, eng, shape, ctx: int, first: int, G, log) -> dict:
+    """Whole edit sessions (ee_edit_step) re-creating the model's own greedy
+    output G from an edited copy, at several edit densities: plain greedy
+    decoding, Reuse with plain greedy steps at edit positions, and Reuse with
+    a 1B-class draft model in the Generate phase (gamma = 7; greedy or
+    entropy-aware verification, k = 5).  Random-init models: the draft model
+    shares no knowledge with the target, so its tokens are rarely accepted;
+    the figures show what the phases cost, not the paper's trained speedups."""
+    from workloads import gen_weights, get_shape, inject_edits, zipf_tokens
+    n = len(G)
+    dshape = get_shape("1b")
+    t0 = time.perf_counter()
+    deng = ee.Engine(dshape, gen_weights(dshape, seed=4321), max_ctx=ctx + n + 80, k_max=64)
+    deng.prefill(0, zipf_tokens(shape.vocab, ctx, seed=42))      # the target's prompt
+    setup = time.perf_counter() - t0
+
+    def run(original, draft, top_k, k_reuse=32):
+        eng.rollback(0, ctx, first)
+        if draft is not None:
+            draft.rollback(0, ctx, first)
+        s = ee.EditSession(eng, 0, original, draft, 0, k_reuse=k_reuse, gamma=7, top_k=top_k, dynamic=True)
+        torch_sync()
+        ts = time.perf_counter()
+        while s.n < n:
+            s.step()
+        el = time.perf_counter() - ts
+        out, st = s.output[:n], s.state
+        return {"tokens_per_s": round(n / el, 1), "seconds": round(el, 3),
+                "steps_reuse": int(st.steps[0]), "steps_generate": int(st.steps[1]),
+                "emitted_reuse": int(st.emitted[0]), "emitted_generate": int(st.emitted[1]),
+                "draft_tokens": int(st.draft_tokens), "equals_greedy_output": out == list(G)}
+
+    res = {"tokens": n, "draft_model": "1b Llama-style random-init bf16", "gamma": 7, "k_reuse": 32,
+           "draft_setup_s": round(setup, 1)}
+    eng.rollback(0, ctx, first)
+    torch_sync()
+    ts = time.perf_counter()
+    for _ in range(n - 1):
+        eng.verify(0, [])
+    ar = (n - 1) / (time.perf_counter() - ts)
+    res["greedy_decoding_tokens_per_s"] = round(ar, 1)
+    for frac in (0.05, 0.25, 0.5):
+        log(f"[bench] edit sessions at edit density {frac}")
+        original, _ = inject_edits(np.asarray(G, dtype=np.int32), shape.vocab, seed=7, frac=frac)
+        row = {"reuse_plus_greedy_steps": run(list(original), None, 0),
+               "reuse_plus_draft_greedy": run(list(original), deng, 0),
+               "reuse_plus_draft_entropy_k5": run(list(original), deng, 5)}
+        for v in row.values():
+            v["speedup_vs_greedy_decoding"] = round(v["tokens_per_s"] / ar, 2)
+        res[f"edit_density_{frac}"] = row
+    deng.close()
+    eng.rollback(0, ctx, first)
+    return res
+
+
+def torch_sync():
+    import torch
+    torch.cuda.synchronize()
+
+
 def attention_flops(s, t: int, n: int) -> int:
     """Score and value products of t rows over n committed keys plus the
     block, in every layer."""
@@ -226,6 +286,7 @@ def main():
     ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
     ap.add_argument("--no-33b", action="store_true", help="skip the 33B batch-of-4 measurement")
     ap.add_argument("--no-long", action="store_true", help="skip the long-draft (K = 128..512) measurement")
+    ap.add_argument("--no-edit", action="store_true", help="skip the edit sessions with a draft model")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -404,6 +465,8 @@ def main():
     eng.profile([])
     eng.rollback(0, ctx, first)
 
+    edit = None if (args.no_edit or args.config != "7b") else edit_sessions(ee, eng, shape, ctx, first, G, log)
+
     result = {
         "metric": METRIC,
         "value": round(emitted / elapsed, 2),
@@ -445,6 +508,7 @@ def main():
         "tree64_at_ctx": tree64,
         "long_drafts_at_ctx": long_drafts or None,
         "entropy_verify_at_ctx": entropy,
+        "edit_sessions": edit,
         "lossless_check": "emitted stream equals the GPU's own greedy output",
     }
     eng.close()
