@@ -302,6 +302,18 @@ int32_t ee_profile(ee_ctx* ctx, uint32_t class_mask);
  * them afterwards. */
 int32_t ee_profile_read(ee_ctx* ctx, double* ms, int64_t* launches, int32_t reset);
 
+/* Measurement aid: the GEMM of one projection (cls = EE_PROF_QKV,
+ * EE_PROF_OPROJ, EE_PROF_GATEUP or EE_PROF_DOWN) launched for every layer in
+ * turn, reps times, back to back on the context's stream, on `rows` rows of
+ * the workspace's current activations (the launch configuration a block of
+ * that many rows uses); *us_per_launch = the elapsed time between two HIP
+ * events around the sequence divided by the launches.  Each launch streams
+ * its own layer's weights, as in a verify step; events around single
+ * launches would add their own overhead to every launch.  Writes only GEMM
+ * partials in the workspace (no sequence state changes).  EE_EINVAL for
+ * another class, rows outside [1, max_seqs * (k_max + 1)] or reps < 1. */
+int32_t ee_time_gemm(ee_ctx* ctx, uint32_t cls, int32_t rows, int32_t reps, double* us_per_launch);
+
 /* Message for the last failed call on ctx (or the last failed context-free
  * call when ctx is NULL).  Never NULL; the pointer stays valid until the next
  * call on the same context. */

@@ -70,6 +70,7 @@ ee_read_kv = _sig("ee_read_kv", _i32, [_vp, _i32, _i32, _vp, _vp])
 ee_last_error = _sig("ee_last_error", ctypes.c_char_p, [_vp])
 ee_profile = _sig("ee_profile", _i32, [_vp, ctypes.c_uint32])
 ee_use_graphs = _sig("ee_use_graphs", _i32, [_vp, _i32])
+ee_time_gemm = _sig("ee_time_gemm", _i32, [_vp, ctypes.c_uint32, _i32, _i32, ctypes.POINTER(ctypes.c_double)])
 ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(ctypes.c_int64), _i32])
 
@@ -310,6 +311,13 @@ class Engine:
         n = (ctypes.c_int64 * len(PROF_CLASSES))()
         _check(ee_profile_read(self.ctx, ms, n, int(reset)), self.ctx)
         return {c: (ms[i], n[i]) for i, c in enumerate(PROF_CLASSES)}
+
+    def time_gemm(self, cls: str, rows: int, reps: int = 3) -> float:
+        """Microseconds per launch of one projection's GEMM, launched for every
+        layer in turn, back to back (ee_time_gemm)."""
+        us = ctypes.c_double()
+        _check(ee_time_gemm(self.ctx, PROF_CLASSES.index(cls), rows, reps, ctypes.byref(us)), self.ctx)
+        return us.value
 
     def close(self):
         if getattr(self, "ctx", None):

@@ -829,6 +829,31 @@ int32_t ee_profile_read(ee_ctx* c, double* ms, int64_t* launches, int32_t reset)
   return EE_OK;
 }
 
+int32_t ee_time_gemm(ee_ctx* c, uint32_t cls, int32_t rows, int32_t reps, double* us_per_launch) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (!us_per_launch || reps < 1) return fail(c, EE_EINVAL, "us_per_launch must be non-NULL and reps >= 1");
+  if (cls != EE_PROF_QKV && cls != EE_PROF_OPROJ && cls != EE_PROF_GATEUP && cls != EE_PROF_DOWN)
+    return fail(c, EE_EINVAL, "class must be one of the four projections");
+  if (rows < 1 || rows > c->lay.Rmax) return fail(c, EE_EINVAL, "rows outside [1, max_seqs * (k_max + 1)]");
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  HIP_TRY(c, hipEventCreate(&e0));
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return fail(c, EE_EHIP, "hipEventCreate");
+  }
+  hipError_t e = hipEventRecord(e0, c->st);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = ee::run_gemm_sequence(c->m, c->w, (int)cls, rows, c->st);
+  if (e == hipSuccess) e = hipEventRecord(e1, c->st);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return hip_fail(c, e, "ee_time_gemm");
+  *us_per_launch = (double)ms * 1e3 / ((double)reps * c->cfg.n_layers);
+  return EE_OK;
+}
+
 const char* ee_last_error(const ee_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
 
 }  // extern "C"

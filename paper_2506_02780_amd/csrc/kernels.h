@@ -115,5 +115,8 @@ enum ProfClass {
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
+// The GEMM of projection `which` (PC_QKV, PC_OPROJ, PC_GATEUP or PC_DOWN) for
+// every layer in turn, on R rows of the current activation buffers (timing).
+hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hipStream_t st);
 
 }  // namespace ee

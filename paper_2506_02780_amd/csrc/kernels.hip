@@ -1530,6 +1530,28 @@ hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, 
   });
 }
 
+hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hipStream_t st) {
+  const int d = m.d, qdim = m.H * m.hd, qkvN = qdim + 2 * m.Hkv * m.hd;
+  for (int l = 0; l < m.L; ++l) {
+    const LayerPtrs& lp = m.layers[l];
+    hipError_t e = hipErrorInvalidValue;
+    const bool bf = m.dt == DT_BF16;
+    switch (which) {
+      case PC_QKV: e = bf ? gemm<DT_BF16>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st)
+                          : gemm<DT_F32>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st); break;
+      case PC_OPROJ: e = bf ? gemm<DT_BF16>(lp.wo, w.xbuf, d, qdim, R, w.part, st)
+                            : gemm<DT_F32>(lp.wo, w.xbuf, d, qdim, R, w.part, st); break;
+      case PC_GATEUP: e = bf ? gemm<DT_BF16>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st)
+                             : gemm<DT_F32>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st); break;
+      case PC_DOWN: e = bf ? gemm<DT_BF16>(lp.wd, w.zbuf, d, m.F, R, w.part, st)
+                           : gemm<DT_F32>(lp.wd, w.zbuf, d, m.F, R, w.part, st); break;
+      default: break;
+    }
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   const size_t layer_elems = (size_t)m.max_pages * 2 * m.Hkv * 64 * m.hd;
   const dim3 grid(m.L * m.Hkv, s.B), block(256);

@@ -56,6 +56,9 @@ def test_null_context_calls_fail_cleanly():
     assert ee.ee_kv_rollback(None, 0, 0, 0) == ee.EE_EINVAL
     assert ee.ee_verify_batch(None, 1, None, None, 0, None, None, None, None) == ee.EE_EINVAL
     assert ee.ee_verify_topk(None, 1, None, None, 0, 3, 1, None, None, None) == ee.EE_EINVAL
+    assert ee.ee_extend(None, 0, None, 0, ctypes.byref(a)) == ee.EE_EINVAL
+    assert ee.ee_time_gemm(None, 5, 1, 1, None) == ee.EE_EINVAL
+    assert ee.ee_edit_begin(None, 0, None, 0, None) == ee.EE_EINVAL
 
 
 def test_matcher_equals_oracle():

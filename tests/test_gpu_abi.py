@@ -65,3 +65,14 @@ def test_rollback_then_regenerate_is_bitwise_identical(ee, eng):
     assert s1 == s2
     np.testing.assert_array_equal(eng.logits(), lg1)
     eng.rollback(0, 0, -1)
+
+
+def test_time_gemm_measurement_aid(ee, eng):
+    us = eng.time_gemm("gateup", 9, reps=2)
+    assert 0.0 < us < 1e5
+    n0 = eng.seq_state(0)
+    for bad in (("attn", 9), ("gateup", 0), ("gateup", 10 ** 6)):
+        with pytest.raises(ee.EEError) as e:
+            eng.time_gemm(*bad)
+        assert e.value.code == ee.EE_EINVAL
+    assert eng.seq_state(0) == n0
