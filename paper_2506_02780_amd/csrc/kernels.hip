@@ -630,26 +630,13 @@ template <int DT, int HD, int THREADS> struct AttnLds {
   static constexpr int PER = (NSUB * UNITS + THREADS - 1) / THREADS;
 };
 
-// One 64-key sub-tile for the wave's 16 query columns: scores S^T = K Q^T
-// (head-dim step outermost, so consecutive MFMAs feed independent
-// accumulators), m = max visible scaled score, l = sum 2^(s-m) and
-// o = sum 2^(s-m) v.  kfn(kt, s) gives the key fragment of key 16kt + c at head
-// dims s*KS + grp*EPL ..; vfn(dt, j) the value fragment of output dims 16dt + c
-// (bf16, j = k2: keys 32j + 4grp + 0..3 then 32j + 16 + 4grp + 0..3; fp32,
-// j = kt: keys 16j + 4grp + 0..3).  Key 16kt + 4grp + r of the sub-tile sits at
-// position base + 16kt + 4grp + r and is visible to a column iff that position
-// is <= the column's own.  A column's result depends only on its query, the
-// key/value data and the positions, never on the other columns.  o is
-// accumulated into (the caller clears it); columns with own == false add
-// exact zeros to it.  vprep(j) runs before the value fragments of PV step j
-// (k2 or kt) are fetched.  STREAMV fetches each value fragment right before
-// its MFMAs (fewer live registers; the same arithmetic in the same order).
-template <int DT, int HD, bool STREAMV, class KFn, class VFn, class VPrep>
-__device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, VFn vfn, VPrep vprep,
-                                              int base, int mypos, float scale_log2, int grp, bool own,
-                                              float& m, float& l, f32x4 (&o)[HD / 16]) {
-  constexpr int NS = HD / Geo<DT>::KS, ND = HD / 16;
-  f32x4 sacc[4];
+// Scores of the sub-tile, S^T = K Q^T (head-dim step outermost, so
+// consecutive MFMAs feed independent accumulators), scaled to log2 units,
+// with keys past the column's position set to -inf; m = their maximum.
+template <int DT, int HD, class KFn>
+__device__ __forceinline__ void subtile_scores(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, int base, int mypos,
+                                               float scale_log2, int grp, f32x4 (&sacc)[4], float& m) {
+  constexpr int NS = HD / Geo<DT>::KS;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -661,7 +648,6 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
     for (int kt = 0; kt < 4; ++kt) sacc[kt] = mma<DT>(kf[kt], qf[s], sacc[kt]);
   }
   m = -INFINITY;
-  l = 0.f;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -673,7 +659,17 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
     }
   m = fmaxf(m, __shfl_xor(m, 16));
   m = fmaxf(m, __shfl_xor(m, 32));
+}
+
+// From the scores and their maximum m: l = sum 2^(s-m) and o += sum 2^(s-m) v
+// (columns with own == false add exact zeros to o).
+template <int DT, int HD, bool STREAMV, class VFn, class VPrep>
+__device__ __forceinline__ void subtile_values(f32x4 (&sacc)[4], float m, VFn vfn, VPrep vprep, int grp, bool own,
+                                               float& l, f32x4 (&o)[HD / 16]) {
+  constexpr int ND = HD / 16;
+  (void)grp;
   const float m_use = m != -INFINITY ? m : 0.f;
+  l = 0.f;
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -731,6 +727,104 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
   }
 }
 
+// One 64-key sub-tile for the wave's 16 query columns: scores S^T = K Q^T
+// (head-dim step outermost, so consecutive MFMAs feed independent
+// accumulators), m = max visible scaled score, l = sum 2^(s-m) and
+// o = sum 2^(s-m) v.  kfn(kt, s) gives the key fragment of key 16kt + c at head
+// dims s*KS + grp*EPL ..; vfn(dt, j) the value fragment of output dims 16dt + c
+// (bf16, j = k2: keys 32j + 4grp + 0..3 then 32j + 16 + 4grp + 0..3; fp32,
+// j = kt: keys 16j + 4grp + 0..3).  Key 16kt + 4grp + r of the sub-tile sits at
+// position base + 16kt + 4grp + r and is visible to a column iff that position
+// is <= the column's own.  A column's result depends only on its query, the
+// key/value data and the positions, never on the other columns.  o is
+// accumulated into (the caller clears it); columns with own == false add
+// exact zeros to it.  vprep(j) runs before the value fragments of PV step j
+// (k2 or kt) are fetched.  STREAMV fetches each value fragment right before
+// its MFMAs (fewer live registers; the same arithmetic in the same order).
+template <int DT, int HD, bool STREAMV, class KFn, class VFn, class VPrep>
+__device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS], KFn kfn, VFn vfn, VPrep vprep,
+                                              int base, int mypos, float scale_log2, int grp, bool own,
+                                              float& m, float& l, f32x4 (&o)[HD / 16]) {
+  f32x4 sacc[4];
+  subtile_scores<DT, HD>(qf, kfn, base, mypos, scale_log2, grp, sacc, m);
+  subtile_values<DT, HD, STREAMV>(sacc, m, vfn, vprep, grp, own, l, o);
+}
+
+// Stage sub-tiles 0 .. nsub-1 of the split starting at position base0 (K rows
+// and V^T, KV head gkv) in LDS with one batch of loads per thread; slots at or
+// past nkeys (not yet written) read as zeros.
+template <int DT, int HD, int THREADS>
+__device__ __forceinline__ void stage_split(const AttnArgs& a, const int* ptable, int gkv, int base0, int nsub,
+                                            int nkeys, unsigned char* lds) {
+  using LY = AttnLds<DT, HD, THREADS>;
+  constexpr int ESZ = Geo<DT>::ESZ;
+  constexpr int ROWB = LY::ROWB, KROW = LY::KROW, VROW = LY::VROW;
+  const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
+  const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
+  constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
+  // the split's NSUB page numbers with one vector load (scalar loads of the
+  // uniform addresses would each wait for the previous one)
+  int pg[NSUB];
+  {
+    static_assert(NSUB == 4, "one 16-byte load of page numbers");
+    const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
+    const uint4 p4 = bload<0>(pr, (unsigned)((base0 >> 6) * 4));
+    pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
+  }
+  uint4 tmp[LY::PER];
+  unsigned dst[LY::PER];
+#pragma unroll
+  for (int j = 0; j < LY::PER; ++j) {
+    const int idx = threadIdx.x + j * THREADS;
+    const int st = idx / LY::UNITS, rem = idx % LY::UNITS;
+    const int kv = rem / HALF, u = rem % HALF;
+    unsigned off = OOB;
+    dst[j] = 0xffffffffu;
+    if (st < nsub) {
+      const int base = base0 + st * 64;
+      int page = pg[0];
+#pragma unroll
+      for (int q = 1; q < NSUB; ++q) page = st == q ? pg[q] : page;
+      const int valid = nkeys - base;
+      off = (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ + (size_t)u * 16);
+      if (kv == 0) {
+        const int row = u / (ROWB / 16), col = u % (ROWB / 16);
+        if (row >= valid) off = OOB;                    // unwritten slots read as zeros
+        dst[j] = st * LY::KSUB + row * KROW + col * 16;
+      } else {
+        constexpr int VU = 64 * ESZ / 16;               // uint4 per V^T row
+        dst[j] = NSUB * LY::KSUB + st * LY::VSUB + (u / VU) * VROW + (u % VU) * 16;
+        dst[j] |= (unsigned)min(valid, 64) << 24;       // remember the valid key count
+      }
+    }
+    tmp[j] = bload<0>(rs, off);
+  }
+#pragma unroll
+  for (int j = 0; j < LY::PER; ++j) {
+    if (dst[j] == 0xffffffffu) continue;
+    unsigned d = dst[j];
+    uint4 v = tmp[j];
+    if ((d >> 24) != 0) {
+      // V^T chunk: zero the key columns of unwritten slots
+      const int valid = (int)(d >> 24);
+      d &= 0x00ffffffu;
+      if (valid < 64) {
+        const int col0 = (((d - NSUB * LY::KSUB) % LY::VSUB) % VROW) / ESZ;
+        uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+        if (DT == DT_BF16) {
+          for (int e = 0; e < 8; ++e)
+            if (col0 + e >= valid) w4[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (col0 + e >= valid) w4[e] = 0;
+        }
+        v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+    }
+    *reinterpret_cast<uint4*>(lds + d) = v;
+  }
+  }
+
 // Split attention.  Workgroup (KV head g, split sp, query-tile group) stages
 // the split's keys and values (positions sp*256 .. sp*256+255, four 64-key
 // sub-tiles) in LDS with one batch of loads; each wave then takes one tile of
@@ -783,82 +877,17 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   const int base = base0 + st * 64;
   uint4 qf[NS];
   {
-    const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.B * a.T * a.H * ROWB));
-    const unsigned qb = (unsigned)(((size_t)(rb + t) * a.H + head) * ROWB);
-    // (tree: waves past the staged sub-tiles may gather, so every wave of a
-    // live query tile needs its queries)
-    const bool need = TREE ? qt < nqt : work;
+  const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.B * a.T * a.H * ROWB));
+  const unsigned qb = (unsigned)(((size_t)(rb + t) * a.H + head) * ROWB);
+  // (tree: waves past the staged sub-tiles may gather, so every wave of a
+  // live query tile needs its queries)
+  const bool need = TREE ? qt < nqt : work;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, (need && colok) ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
+  for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, (need && colok) ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
   }
 
   // ---- stage every sub-tile of the split with one batch of loads ----
-  {
-    const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
-    const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
-    constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
-    // the split's NSUB page numbers with one vector load (scalar loads of the
-    // uniform addresses would each wait for the previous one)
-    int pg[NSUB];
-    {
-      static_assert(NSUB == 4, "one 16-byte load of page numbers");
-      const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
-      const uint4 p4 = bload<0>(pr, (unsigned)((base0 >> 6) * 4));
-      pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
-    }
-    uint4 tmp[LY::PER];
-    unsigned dst[LY::PER];
-#pragma unroll
-    for (int j = 0; j < LY::PER; ++j) {
-      const int idx = threadIdx.x + j * ATT_THREADS;
-      const int st = idx / LY::UNITS, rem = idx % LY::UNITS;
-      const int kv = rem / HALF, u = rem % HALF;
-      unsigned off = OOB;
-      dst[j] = 0xffffffffu;
-      if (st < nsub) {
-        const int base = base0 + st * 64;
-        int page = pg[0];
-#pragma unroll
-        for (int q = 1; q < NSUB; ++q) page = st == q ? pg[q] : page;
-        const int valid = nkeys - base;
-        off = (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ + (size_t)u * 16);
-        if (kv == 0) {
-          const int row = u / (ROWB / 16), col = u % (ROWB / 16);
-          if (row >= valid) off = OOB;                    // unwritten slots read as zeros
-          dst[j] = st * LY::KSUB + row * KROW + col * 16;
-        } else {
-          constexpr int VU = 64 * ESZ / 16;               // uint4 per V^T row
-          dst[j] = NSUB * LY::KSUB + st * LY::VSUB + (u / VU) * VROW + (u % VU) * 16;
-          dst[j] |= (unsigned)min(valid, 64) << 24;       // remember the valid key count
-        }
-      }
-      tmp[j] = bload<0>(rs, off);
-    }
-#pragma unroll
-    for (int j = 0; j < LY::PER; ++j) {
-      if (dst[j] == 0xffffffffu) continue;
-      unsigned d = dst[j];
-      uint4 v = tmp[j];
-      if ((d >> 24) != 0) {
-        // V^T chunk: zero the key columns of unwritten slots
-        const int valid = (int)(d >> 24);
-        d &= 0x00ffffffu;
-        if (valid < 64) {
-          const int col0 = (((d - NSUB * LY::KSUB) % LY::VSUB) % VROW) / ESZ;
-          uint32_t w4[4] = {v.x, v.y, v.z, v.w};
-          if (DT == DT_BF16) {
-            for (int e = 0; e < 8; ++e)
-              if (col0 + e >= valid) w4[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-          } else {
-            for (int e = 0; e < 4; ++e)
-              if (col0 + e >= valid) w4[e] = 0;
-          }
-          v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
-        }
-      }
-      *reinterpret_cast<uint4*>(lds + d) = v;
-    }
-  }
+  stage_split<DT, HD, ATT_THREADS>(a, ptable, gkv, base0, nsub, nkeys, lds);
   __syncthreads();
 
   // A tree row at depth j sits at position n + j and sees, at positions
@@ -873,15 +902,15 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   // is empty), each serving one gather sub-tile and a share of the rows.
   int g0 = 0, g1 = -1;
   if (TREE) {
-    int mx = mypos;
-    mx = max(mx, __shfl_xor(mx, 1));
-    mx = max(mx, __shfl_xor(mx, 2));
-    mx = max(mx, __shfl_xor(mx, 4));
-    mx = max(mx, __shfl_xor(mx, 8));   // uniform: the query tile's largest position
-    if (mx > n && mx >= base0) {
-      g0 = n + 1 >= base0 ? (n + 1 - base0) >> 6 : 0;
-      g1 = min(nsub - 1, (mx - base0) >> 6);
-    }
+  int mx = mypos;
+  mx = max(mx, __shfl_xor(mx, 1));
+  mx = max(mx, __shfl_xor(mx, 2));
+  mx = max(mx, __shfl_xor(mx, 4));
+  mx = max(mx, __shfl_xor(mx, 8));   // uniform: the query tile's largest position
+  if (mx > n && mx >= base0) {
+    g0 = n + 1 >= base0 ? (n + 1 - base0) >> 6 : 0;
+    g1 = min(nsub - 1, (mx - base0) >> 6);
+  }
   }
   const bool worker = TREE && g1 >= g0 && st >= g0;
 
@@ -890,21 +919,21 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < ND; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (work && !worker) {
-    const unsigned char* Ks = Kall + st * LY::KSUB;
-    const unsigned char* Vt = Vall + st * LY::VSUB;
-    auto kfn = [&](int kt, int s) {
-      return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
-    };
-    auto vfn = [&](int dt, int j) {
-      const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-      if (DT == DT_BF16) {
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
-        return make_uint4(lo.x, lo.y, hi.x, hi.y);
-      }
-      return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
-    };
-    subtile_state<DT, HD, false>(qf, kfn, vfn, [](int) {}, base, mypos, a.scale_log2, grp, true, m, l, o);
+  const unsigned char* Ks = Kall + st * LY::KSUB;
+  const unsigned char* Vt = Vall + st * LY::VSUB;
+  auto kfn = [&](int kt, int s) {
+    return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+  };
+  auto vfn = [&](int dt, int j) {
+    const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
+    if (DT == DT_BF16) {
+      const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
+      const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+    return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
+  };
+  subtile_state<DT, HD, false>(qf, kfn, vfn, [](int) {}, base, mypos, a.scale_log2, grp, true, m, l, o);
   }
 
   // a gathering wave serves sub-tile g0 + gi (positions n+1 .. n+64 span at
@@ -915,139 +944,139 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   const int gi = worker ? wk % ng : 0, kk = worker ? wk / ng : 0;
   const int nw = worker ? (NSUB - g0 - gi + ng - 1) / ng : 1;
   if (worker && qt < nqt && t_lo + kk <= t_hi) {
-    const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
-    const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
-    // Gathered slots never precede the sub-tile: a committed key keeps its
-    // position, and the ancestor shown at position n + j is a block row of
-    // index >= j, i.e. slot >= n + j.  So when the block ends inside the staged
-    // split (the usual case) every gathered slot is staged: gather from LDS;
-    // else from the KV pool.  Uniform over the workgroup.
-    const bool from_lds = nkeys <= base0 + 64 * nsub;
-    // pages of the slots a gather sub-tile can touch, [base0 + 64 g0, n + T):
-    // at most four 64-slot pages, fetched once
-    const int pw0 = (base0 >> 6) + g0;
-    int pgt[4];
+  const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
+  const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
+  // Gathered slots never precede the sub-tile: a committed key keeps its
+  // position, and the ancestor shown at position n + j is a block row of
+  // index >= j, i.e. slot >= n + j.  So when the block ends inside the staged
+  // split (the usual case) every gathered slot is staged: gather from LDS;
+  // else from the KV pool.  Uniform over the workgroup.
+  const bool from_lds = nkeys <= base0 + 64 * nsub;
+  // pages of the slots a gather sub-tile can touch, [base0 + 64 g0, n + T):
+  // at most four 64-slot pages, fetched once
+  const int pw0 = (base0 >> 6) + g0;
+  int pgt[4];
+  {
+    const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
+    const unsigned o4 = (unsigned)(pw0 * 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pgt[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(pr, o4 + 4 * i, 0, 0);
+  }
+  // row tr's path (lane j holds the block row at depth j + 1) and position;
+  // the next row's are fetched while the current one is computed
+  const auto pathr = make_rsrc(path, (unsigned)(a.T * 64));
+  const auto posr = make_rsrc(pos, (unsigned)(a.T * 4));
+  int tr = t_lo + kk;
+  uint32_t pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)(tr * 64 + lane), 0, 0);
+  int ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)(tr * 4), 0, 0);
+  for (; tr <= t_hi; tr += nw) {
+    const int dep = __builtin_amdgcn_readfirstlane(ptr) - n;
+    const int pth_tr = (int)pth;
+    if (tr + nw <= t_hi) {
+      pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)((tr + nw) * 64 + lane), 0, 0);
+      ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)((tr + nw) * 4), 0, 0);
+    }
+    // physical slot holding position kp on row tr's path (-1: hidden); the
+    // lane shuffle runs on every lane
+    auto slot_of = [&](int kp) {
+      const int j = min(max(kp - n - 1, 0), 63);
+      const int anc = n + (__shfl(pth_tr, j) & 0xff);
+      return kp <= n ? kp : (kp - n <= dep ? anc : -1);
+    };
+    // every column accumulates; only row tr's columns get non-zero weights
+    const bool own = colok && t == tr;
+    constexpr int NVK = DT == DT_BF16 ? 8 : 4;   // value keys of one PV step per lane
+    // value key i of PV step j: bf16 32j + 16(i/4) + 4grp + i%4, fp32 16j + 4grp + i
+    auto vkey = [&](int j, int i) {
+      return DT == DT_BF16 ? 32 * j + 16 * (i >> 2) + 4 * grp + (i & 3) : 16 * j + 4 * grp + i;
+    };
     {
-      const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
-      const unsigned o4 = (unsigned)(pw0 * 4);
+      const int gbase = base0 + 64 * (g0 + gi);
+      float mt, lt;
+      if (from_lds) {
+        // staged row of each key; hidden keys (weight 0) read a staged row
+        auto row_of = [&](int kp) {
+          const int ps = slot_of(kp);
+          return (ps < 0 ? max(n, base0) : ps) - base0;
+        };
+        int krow[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pgt[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(pr, o4 + 4 * i, 0, 0);
-    }
-    // row tr's path (lane j holds the block row at depth j + 1) and position;
-    // the next row's are fetched while the current one is computed
-    const auto pathr = make_rsrc(path, (unsigned)(a.T * 64));
-    const auto posr = make_rsrc(pos, (unsigned)(a.T * 4));
-    int tr = t_lo + kk;
-    uint32_t pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)(tr * 64 + lane), 0, 0);
-    int ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)(tr * 4), 0, 0);
-    for (; tr <= t_hi; tr += nw) {
-      const int dep = __builtin_amdgcn_readfirstlane(ptr) - n;
-      const int pth_tr = (int)pth;
-      if (tr + nw <= t_hi) {
-        pth = __builtin_amdgcn_raw_buffer_load_b8(pathr, (unsigned)((tr + nw) * 64 + lane), 0, 0);
-        ptr = (int)__builtin_amdgcn_raw_buffer_load_b32(posr, (unsigned)((tr + nw) * 4), 0, 0);
+        for (int kt = 0; kt < 4; ++kt) krow[kt] = row_of(gbase + 16 * kt + c);
+        auto kfn = [&](int kt, int s) {
+          const int r = krow[kt];
+          return *reinterpret_cast<const uint4*>(Kall + (r >> 6) * LY::KSUB + (r & 63) * KROW +
+                                                 (s * KS + grp * EPL) * ESZ);
+        };
+        int vrow[NVK];
+        auto vprep = [&](int j) {
+#pragma unroll
+          for (int i = 0; i < NVK; ++i) vrow[i] = row_of(gbase + vkey(j, i));
+        };
+        auto vfn = [&](int dt, int j) {
+          const unsigned char* vd = Vall + (16 * dt + c) * VROW;
+          auto elt = [&](int i) -> uint32_t {
+            const int r = vrow[i];
+            const unsigned char* src = vd + (r >> 6) * LY::VSUB + (r & 63) * ESZ;
+            return DT == DT_BF16 ? (uint32_t)*reinterpret_cast<const uint16_t*>(src)
+                                 : *reinterpret_cast<const uint32_t*>(src);
+          };
+          uint32_t w[4];
+          if (DT == DT_BF16) {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) w[h] = elt(2 * h) | (elt(2 * h + 1) << 16);
+          } else {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) w[h] = elt(h);
+          }
+          return make_uint4(w[0], w[1], w[2], w[3]);
+        };
+        subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
+      } else {
+        // byte offset in the KV pool of slot ps's K row (kv = 0) or V^T column (kv = 1)
+        auto off_of = [&](int ps, int kv) {
+          if (ps < 0) return OOB;
+          const int pi = (ps >> 6) - pw0;             // 0..3 (see pw0)
+          const int page = pi == 0 ? pgt[0] : pi == 1 ? pgt[1] : pi == 2 ? pgt[2] : pgt[3];
+          return (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ +
+                            (size_t)(ps & 63) * (kv ? 1 : HD) * ESZ);
+        };
+        unsigned koff[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) koff[kt] = off_of(slot_of(gbase + 16 * kt + c), 0);
+        auto kfn = [&](int kt, int s) {
+          return bload<0>(rs, koff[kt] == OOB ? OOB : koff[kt] + (unsigned)((s * KS + grp * EPL) * ESZ));
+        };
+        unsigned voff[NVK];
+        auto vprep = [&](int j) {
+#pragma unroll
+          for (int i = 0; i < NVK; ++i) voff[i] = off_of(slot_of(gbase + vkey(j, i)), 1);
+        };
+        auto vfn = [&](int dt, int j) {
+          const unsigned drow = (unsigned)((16 * dt + c) * 64 * ESZ);
+          auto elt = [&](int i) -> uint32_t {
+            const unsigned off = voff[i] == OOB ? OOB : voff[i] + drow;
+            return DT == DT_BF16 ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0)
+                                 : __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+          };
+          uint32_t w[4];
+          if (DT == DT_BF16) {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) w[h] = (elt(2 * h) & 0xffffu) | (elt(2 * h + 1) << 16);
+          } else {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) w[h] = elt(h);
+          }
+          return make_uint4(w[0], w[1], w[2], w[3]);
+        };
+        // all value fragments of a PV step are fetched before its MFMAs
+        subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
       }
-      // physical slot holding position kp on row tr's path (-1: hidden); the
-      // lane shuffle runs on every lane
-      auto slot_of = [&](int kp) {
-        const int j = min(max(kp - n - 1, 0), 63);
-        const int anc = n + (__shfl(pth_tr, j) & 0xff);
-        return kp <= n ? kp : (kp - n <= dep ? anc : -1);
-      };
-      // every column accumulates; only row tr's columns get non-zero weights
-      const bool own = colok && t == tr;
-      constexpr int NVK = DT == DT_BF16 ? 8 : 4;   // value keys of one PV step per lane
-      // value key i of PV step j: bf16 32j + 16(i/4) + 4grp + i%4, fp32 16j + 4grp + i
-      auto vkey = [&](int j, int i) {
-        return DT == DT_BF16 ? 32 * j + 16 * (i >> 2) + 4 * grp + (i & 3) : 16 * j + 4 * grp + i;
-      };
-      {
-        const int gbase = base0 + 64 * (g0 + gi);
-        float mt, lt;
-        if (from_lds) {
-          // staged row of each key; hidden keys (weight 0) read a staged row
-          auto row_of = [&](int kp) {
-            const int ps = slot_of(kp);
-            return (ps < 0 ? max(n, base0) : ps) - base0;
-          };
-          int krow[4];
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt) krow[kt] = row_of(gbase + 16 * kt + c);
-          auto kfn = [&](int kt, int s) {
-            const int r = krow[kt];
-            return *reinterpret_cast<const uint4*>(Kall + (r >> 6) * LY::KSUB + (r & 63) * KROW +
-                                                   (s * KS + grp * EPL) * ESZ);
-          };
-          int vrow[NVK];
-          auto vprep = [&](int j) {
-#pragma unroll
-            for (int i = 0; i < NVK; ++i) vrow[i] = row_of(gbase + vkey(j, i));
-          };
-          auto vfn = [&](int dt, int j) {
-            const unsigned char* vd = Vall + (16 * dt + c) * VROW;
-            auto elt = [&](int i) -> uint32_t {
-              const int r = vrow[i];
-              const unsigned char* src = vd + (r >> 6) * LY::VSUB + (r & 63) * ESZ;
-              return DT == DT_BF16 ? (uint32_t)*reinterpret_cast<const uint16_t*>(src)
-                                   : *reinterpret_cast<const uint32_t*>(src);
-            };
-            uint32_t w[4];
-            if (DT == DT_BF16) {
-#pragma unroll
-              for (int h = 0; h < 4; ++h) w[h] = elt(2 * h) | (elt(2 * h + 1) << 16);
-            } else {
-#pragma unroll
-              for (int h = 0; h < 4; ++h) w[h] = elt(h);
-            }
-            return make_uint4(w[0], w[1], w[2], w[3]);
-          };
-          subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
-        } else {
-          // byte offset in the KV pool of slot ps's K row (kv = 0) or V^T column (kv = 1)
-          auto off_of = [&](int ps, int kv) {
-            if (ps < 0) return OOB;
-            const int pi = (ps >> 6) - pw0;             // 0..3 (see pw0)
-            const int page = pi == 0 ? pgt[0] : pi == 1 ? pgt[1] : pi == 2 ? pgt[2] : pgt[3];
-            return (unsigned)(((((size_t)page * 2 + kv) * a.Hkv + gkv) * 64 * HD) * ESZ +
-                              (size_t)(ps & 63) * (kv ? 1 : HD) * ESZ);
-          };
-          unsigned koff[4];
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt) koff[kt] = off_of(slot_of(gbase + 16 * kt + c), 0);
-          auto kfn = [&](int kt, int s) {
-            return bload<0>(rs, koff[kt] == OOB ? OOB : koff[kt] + (unsigned)((s * KS + grp * EPL) * ESZ));
-          };
-          unsigned voff[NVK];
-          auto vprep = [&](int j) {
-#pragma unroll
-            for (int i = 0; i < NVK; ++i) voff[i] = off_of(slot_of(gbase + vkey(j, i)), 1);
-          };
-          auto vfn = [&](int dt, int j) {
-            const unsigned drow = (unsigned)((16 * dt + c) * 64 * ESZ);
-            auto elt = [&](int i) -> uint32_t {
-              const unsigned off = voff[i] == OOB ? OOB : voff[i] + drow;
-              return DT == DT_BF16 ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0)
-                                   : __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
-            };
-            uint32_t w[4];
-            if (DT == DT_BF16) {
-#pragma unroll
-              for (int h = 0; h < 4; ++h) w[h] = (elt(2 * h) & 0xffffu) | (elt(2 * h + 1) << 16);
-            } else {
-#pragma unroll
-              for (int h = 0; h < 4; ++h) w[h] = elt(h);
-            }
-            return make_uint4(w[0], w[1], w[2], w[3]);
-          };
-          // all value fragments of a PV step are fetched before its MFMAs
-          subtile_state<DT, HD, false>(qf, kfn, vfn, vprep, gbase, mypos, a.scale_log2, grp, own, mt, lt, o);
-        }
-        if (own) {
-          m = mt;
-          l = lt;
-        }
+      if (own) {
+        m = mt;
+        l = lt;
       }
     }
+  }
   }
 
   // sub-tile states -> LDS (over the staged keys, no longer needed); merge in
@@ -1059,26 +1088,26 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   float* stM = stO + ATT_QT * NSUB * HD * 17;                           // [ATT_QT][NSUB][16]
   float* stL = stM + ATT_QT * NSUB * 16;
   auto put_state = [&](int slot, const f32x4 (&ov)[ND], float mv, float lv) {
-    float* so = stO + ((size_t)(qi * NSUB + slot) * HD) * 17;
+  float* so = stO + ((size_t)(qi * NSUB + slot) * HD) * 17;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt)
+  for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = ov[dt][r];
-    if (grp == 0) {
-      stM[(qi * NSUB + slot) * 16 + c] = mv;
-      stL[(qi * NSUB + slot) * 16 + c] = lv;
-    }
+    for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = ov[dt][r];
+  if (grp == 0) {
+    stM[(qi * NSUB + slot) * 16 + c] = mv;
+    stL[(qi * NSUB + slot) * 16 + c] = lv;
+  }
   };
   if (!worker) {
-    put_state(st, o, m, l);
+  put_state(st, o, m, l);
   } else {
-    if (st > g1) {
-      f32x4 z[ND];
+  if (st > g1) {
+    f32x4 z[ND];
 #pragma unroll
-      for (int i = 0; i < ND; ++i) z[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-      put_state(st, z, -INFINITY, 0.f);
-    }
-    if (qt < nqt && colok && t >= t_lo + kk && (t - t_lo - kk) % nw == 0) put_state(g0 + gi, o, m, l);
+    for (int i = 0; i < ND; ++i) z[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    put_state(st, z, -INFINITY, 0.f);
+  }
+  if (qt < nqt && colok && t >= t_lo + kk && (t - t_lo - kk) % nw == 0) put_state(g0 + gi, o, m, l);
   }
   __syncthreads();
   // thread -> (query tile, column, HD/16 dims)
@@ -1090,27 +1119,136 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   float M = -INFINITY;
 #pragma unroll
   for (int j = 0; j < NSUB; ++j)
-    if (stL[(mq * NSUB + j) * 16 + col] > 0.f) M = fmaxf(M, stM[(mq * NSUB + j) * 16 + col]);
+  if (stL[(mq * NSUB + j) * 16 + col] > 0.f) M = fmaxf(M, stM[(mq * NSUB + j) * 16 + col]);
   float L = 0.f, O[DPT];
 #pragma unroll
   for (int e = 0; e < DPT; ++e) O[e] = 0.f;
 #pragma unroll
   for (int j = 0; j < NSUB; ++j) {
-    const float lj = stL[(mq * NSUB + j) * 16 + col];
-    if (!(lj > 0.f)) continue;
-    const float w = exp2f(stM[(mq * NSUB + j) * 16 + col] - M);
-    L = fmaf(lj, w, L);
-    const float* so = stO + ((size_t)(mq * NSUB + j) * HD + d0) * 17 + col;
+  const float lj = stL[(mq * NSUB + j) * 16 + col];
+  if (!(lj > 0.f)) continue;
+  const float w = exp2f(stM[(mq * NSUB + j) * 16 + col] - M);
+  L = fmaf(lj, w, L);
+  const float* so = stO + ((size_t)(mq * NSUB + j) * HD + d0) * 17 + col;
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) O[e] = fmaf(so[e * 17], w, O[e]);
+  for (int e = 0; e < DPT; ++e) O[e] = fmaf(so[e * 17], w, O[e]);
   }
   float* out = a.part + (((size_t)sp * a.Hkv + gkv) * ((size_t)a.B * a.ncols) + (size_t)b * a.ncols + qcol) * (HD + 2);
 #pragma unroll
   for (int e = 0; e < DPT; e += 4)
-    *reinterpret_cast<float4*>(out + d0 + e) = make_float4(O[e], O[e + 1], O[e + 2], O[e + 3]);
+  *reinterpret_cast<float4*>(out + d0 + e) = make_float4(O[e], O[e + 1], O[e + 2], O[e + 3]);
   if (d0 == 0) {
-    out[HD] = M;
-    out[HD + 1] = L;
+  out[HD] = M;
+  out[HD + 1] = L;
+  }
+}
+
+// Split attention for blocks with many query tiles (long drafts, batches of
+// sequences).  Workgroup (KV head g, split sp, sequence b, group qg of nqg)
+// stages the split once and its 8 waves walk the sequence's query tiles qg*8 +
+// wave, + 8 nqg, ...; a wave computes all four sub-tiles of a query tile
+// itself: the scores of every sub-tile first (their maxima give the split
+// maximum M), then each sub-tile's weights and value products, folded in
+// sub-tile order with weight 2^(m_j - M).  Every operation on a column's
+// values is the one attn_kernel performs (same sub-tile arithmetic, same merge
+// order), so the two kernels give bitwise equal states; this one only avoids
+// staging the split again for every four query tiles.
+constexpr int WIDE_THREADS = 512;
+constexpr int WIDE_MIN_QT = 24;   // query tiles per sequence from which the wide kernel is used
+
+template <int DT, int HD>
+__global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int nqg) {
+  using LY = AttnLds<DT, HD, WIDE_THREADS>;
+  constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
+  constexpr int NS = HD / KS, ND = HD / 16;
+  constexpr int ROWB = LY::ROWB, KROW = LY::KROW, VROW = LY::VROW;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LY::KV_BYTES];
+  const unsigned char* Kall = lds;
+  const unsigned char* Vall = lds + NSUB * LY::KSUB;
+
+  const int nqt = (a.ncols + 15) / 16;
+  const int gkv = blockIdx.x, sp = blockIdx.y, b = blockIdx.z / nqg, qg = blockIdx.z % nqg;
+  const int rb = b * a.T;
+  const int* pos = a.pos + rb;
+  const int* ptable = a.ptable + b * a.ptable_len;
+  const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
+  const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
+  if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int grp = lane >> 4, c = lane & 15;
+  const int nkeys = n + a.T;
+  const int base0 = sp * SPLIT;
+  const int nsub = min(NSUB, (nkeys - base0 + 63) / 64);
+  stage_split<DT, HD, WIDE_THREADS>(a, ptable, gkv, base0, nsub, nkeys, lds);
+  __syncthreads();
+
+  const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.B * a.T * a.H * ROWB));
+  for (int qt = qg * 8 + wv; qt < nqt; qt += nqg * 8) {   // uniform per wave
+    const int qc = qt * 16 + c;
+    const bool colok = qc < a.ncols;
+    const int t = colok ? qc / a.G : 0;
+    const int head = gkv * a.G + (colok ? qc % a.G : 0);
+    const int mypos = colok ? pos[t] : -1;
+    uint4 qf[NS];
+    const unsigned qb = (unsigned)(((size_t)(rb + t) * a.H + head) * ROWB);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[s] = bload<0>(qr, colok ? qb + (unsigned)((s * KS + grp * EPL) * ESZ) : OOB);
+    f32x4 sc[NSUB][4];
+    float mj[NSUB];
+    float M = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st) {
+      mj[st] = -INFINITY;
+      if (st < nsub) {
+        const unsigned char* Ks = Kall + st * LY::KSUB;
+        auto kfn = [&](int kt, int s) {
+          return *reinterpret_cast<const uint4*>(Ks + (size_t)(16 * kt + c) * KROW + (s * KS + grp * EPL) * ESZ);
+        };
+        subtile_scores<DT, HD>(qf, kfn, base0 + st * 64, mypos, a.scale_log2, grp, sc[st], mj[st]);
+      }
+      if (mj[st] > -INFINITY && mj[st] < INFINITY) M = fmaxf(M, mj[st]);
+    }
+    float L = 0.f;
+    f32x4 O[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) O[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st) {
+      if (st >= nsub) continue;
+      const unsigned char* Vt = Vall + st * LY::VSUB;
+      auto vfn = [&](int dt, int j) {
+        const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
+        if (DT == DT_BF16) {
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
+          return make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+        return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
+      };
+      f32x4 oj[ND];
+#pragma unroll
+      for (int i = 0; i < ND; ++i) oj[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      float lj;
+      subtile_values<DT, HD, false>(sc[st], mj[st], vfn, [](int) {}, grp, true, lj, oj);
+      if (lj > 0.f) {
+        const float w = exp2f(mj[st] - M);
+        L = fmaf(lj, w, L);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) O[dt][r] = fmaf(oj[dt][r], w, O[dt][r]);
+      }
+    }
+    if (colok) {
+      float* out = a.part + (((size_t)sp * a.Hkv + gkv) * ((size_t)a.B * a.ncols) + (size_t)b * a.ncols + qc) * (HD + 2);
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt)
+        *reinterpret_cast<float4*>(out + 16 * dt + 4 * grp) = make_float4(O[dt][0], O[dt][1], O[dt][2], O[dt][3]);
+      if (grp == 0) {
+        out[HD] = M;
+        out[HD + 1] = L;
+      }
+    }
   }
 }
 
@@ -1446,6 +1584,15 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if ((e = timed(prof, PC_ATTN, st, [&] {
            // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
            const int qt = att_qt(aa.tree);
+           if (!aa.tree && nqt >= WIDE_MIN_QT) {
+             // many query tiles: stage each split once per group of them; the
+             // groups per sequence keep about two workgroups per CU in flight
+             const int per = m.Hkv * nsplit * B;
+             const int nqg = std::max(1, std::min((nqt + 7) / 8, (512 + per - 1) / per));
+             hipLaunchKernelGGL((attn_wide_kernel<DT, HD>), dim3(m.Hkv, nsplit, B * nqg), dim3(WIDE_THREADS), 0, st,
+                                aa, nqg);
+             return last();
+           }
            const dim3 grid(m.Hkv, nsplit, B * ((nqt + qt - 1) / qt));
            if (aa.tree)
              hipLaunchKernelGGL((attn_kernel<DT, HD, true>), grid, dim3(att_threads(true)), 0, st, aa);

@@ -148,3 +148,31 @@ def test_trees_stay_within_64_nodes(ee):
     a, _, nodes = eng.verify(0, list(range(64)), list(range(-1, 63)))   # a 64-node chain is fine
     assert eng.seq_state(0)[0] == before[0] + 1 + a
     eng.close()
+
+
+def test_long_batch_rows_equal_single_sequence_rows_bitwise(ee):
+    """Two sequences with 200-token drafts in one block (wide attention and
+    row-group GEMMs) equal each sequence verified alone, bit for bit."""
+    shape = _bf16_small()
+    w = gen_weights(shape, seed=95, std=0.05)
+    prompts = [zipf_tokens(shape.vocab, n, seed=9 + n) for n in (90, 333)]
+    eng = ee.Engine(shape, w, max_ctx=1024, max_seqs=2, k_max=256)
+    for b, p in enumerate(prompts):
+        eng.prefill(b, p)
+    states = [eng.seq_state(b) for b in range(2)]
+    drafts = [zipf_tokens(shape.vocab, 200, seed=20 + b) for b in range(2)]
+    single = []
+    for b in range(2):
+        res = eng.verify(b, drafts[b])
+        single.append((res[:2], eng.logits(), [eng.read_kv(b, l) for l in range(shape.n_layers)]))
+        eng.rollback(b, *states[b])
+    res = eng.verify_batch([1, 0], [drafts[1], drafts[0]])
+    lg = eng.logits()
+    for i, b in enumerate((1, 0)):
+        assert res[i][:2] == single[b][0]
+        np.testing.assert_array_equal(lg[i * 201:(i + 1) * 201], single[b][1])
+        for l in range(shape.n_layers):
+            k, v = eng.read_kv(b, l)
+            np.testing.assert_array_equal(k, single[b][2][l][0])
+            np.testing.assert_array_equal(v, single[b][2][l][1])
+    eng.close()
