@@ -24,6 +24,8 @@ What it computes (all arithmetic in float64):
 * ``match`` - the prefix/suffix matcher that resumes Reuse (Sec. "Reuse").
 * ``session`` - prefill / verify / rollback / plain greedy decoding (Eq. 1)
   over an oracle-owned KV cache.
+* ``sampling`` - stochastic speculative sampling (Eq. 4) with the draws
+  given as inputs.
 * ``driver`` - the Reuse / Generate phase machine of an edit session with an
   optional draft model.
 """
@@ -35,10 +37,11 @@ from .entropy import accept_topk, entropy_threshold, topk_tokens
 from .match import match_reuse
 from .session import OracleSession
 from .driver import OracleEditSession
+from .sampling import accept_sample, sample_index, target_probs
 
 __all__ = [
     "round_bf16", "forward_block", "chain_structure", "tree_structure",
     "greedy_rows", "accept_linear", "accept_tree", "top2_margin", "match_reuse",
     "accept_topk", "entropy_threshold", "topk_tokens",
-    "OracleSession", "OracleEditSession",
+    "OracleSession", "OracleEditSession", "accept_sample", "sample_index", "target_probs",
 ]

@@ -176,3 +176,36 @@ def test_long_batch_rows_equal_single_sequence_rows_bitwise(ee):
             np.testing.assert_array_equal(k, single[b][2][l][0])
             np.testing.assert_array_equal(v, single[b][2][l][1])
     eng.close()
+
+
+def test_extend_commits_every_row_and_matches_oracle(ee):
+    """ee_extend: [pending, tokens...] committed without verification, in
+    blocks of k_max + 1 rows; the new pending token and the cache match the
+    oracle, and n = 0 is a plain greedy step."""
+    shape = get_shape("tiny")
+    w = gen_weights(shape, seed=96, std=0.1)
+    prompt = zipf_tokens(shape.vocab, 30, seed=2)
+    ref = OracleSession(shape, w)
+    ref.prefill(prompt)
+    eng = ee.Engine(shape, w, max_ctx=512, k_max=16)
+    eng.prefill(0, prompt)
+    for n in (0, 5, 16, 17, 40):          # 40 rows + pending: three blocks of <= 17 rows
+        toks = zipf_tokens(shape.vocab, n, seed=n + 3)
+        assert eng.extend(0, toks) == ref.extend(toks)
+        assert eng.seq_state(0) == (ref.n, ref.pending)
+    for l in range(shape.n_layers):
+        k, v = eng.read_kv(0, l)
+        np.testing.assert_allclose(k, ref.cache[l][0], rtol=0, atol=2e-5)
+        np.testing.assert_allclose(v, ref.cache[l][1], rtol=0, atol=2e-5)
+    n0, p0 = eng.seq_state(0)
+    a, nxt, _ = eng.verify(0, [])
+    eng.rollback(0, n0, p0)
+    assert eng.extend(0, []) == nxt
+    with pytest.raises(ee.EEError) as e:
+        eng.extend(0, [shape.vocab])
+    assert e.value.code == ee.EE_EINVAL
+    with pytest.raises(ee.EEError) as e:
+        eng.extend(0, [1] * 600)          # past max_ctx: nothing committed
+    assert e.value.code == ee.EE_ECAPACITY
+    assert eng.seq_state(0) == (n0 + 1, nxt)
+    eng.close()
