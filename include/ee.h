@@ -174,6 +174,25 @@ int32_t ee_verify_topk(ee_ctx* ctx, int32_t n_seq, const int32_t* seqs, const in
                        int32_t K, int32_t top_k, int32_t dynamic, int32_t* accept_lens,
                        int32_t* next_tokens, int32_t* thresholds);
 
+/* Stochastic speculative verification (Sec. "Speculative Decoding", Eq. 4)
+ * of a linear draft for one sequence.  Row i's target distribution is
+ * p_i = softmax(logits_i / temperature); draft token d_{i+1} is accepted when
+ * eps[i] * q_i[d_{i+1}] < p_i[d_{i+1}] (eps[i] < p / q), with q_dev the draft
+ * model's distributions (device memory, fp32 [K][vocab], row i = the
+ * distribution d_{i+1} was drawn from; NULL = a greedy draft, q one-hot at
+ * the drafted token).  At the first rejected row a the next token is drawn
+ * from max(0, p_a - q_a) renormalised (residual != 0; the output then follows
+ * p exactly) or from p_a (residual == 0); with every draft token accepted it
+ * is drawn from p_K.  A draw takes the smallest token whose cumulative weight
+ * (token order) exceeds u[a] times the total.  eps (K values) and u (K + 1
+ * values) are host arrays of uniform draws in [0, 1) supplied by the caller,
+ * so a call is reproducible.  Probabilities are computed in float64 from the
+ * float32 logits.  Effects as ee_verify.  Errors: as ee_verify, plus
+ * EE_EINVAL for a draw outside [0, 1) or temperature <= 0. */
+int32_t ee_verify_sample(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t K,
+                         const float* q_dev, const float* eps, const float* u, float temperature,
+                         int32_t residual, int32_t* accept_len, int32_t* next_token);
+
 /* Truncate sequence `seq` to its first new_len committed positions
  * (new_len <= len), release pages wholly beyond them and make pending_token
  * pending.  new_len == 0 with pending_token == -1 empties the sequence (it

@@ -61,6 +61,9 @@ ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_batch = _sig("ee_verify_batch", _i32, [_vp, _i32, _pi32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_topk = _sig("ee_verify_topk", _i32, [_vp, _i32, _pi32, _pi32, _i32, _i32, _i32, _pi32, _pi32, _pi32])
+_pf32 = ctypes.POINTER(ctypes.c_float)
+ee_verify_sample = _sig("ee_verify_sample", _i32, [_vp, _i32, _pi32, _i32, _vp, _pf32, _pf32, ctypes.c_float, _i32,
+                                                   _pi32, _pi32])
 ee_extend = _sig("ee_extend", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_kv_rollback = _sig("ee_kv_rollback", _i32, [_vp, _i32, _i32, _i32])
 ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
@@ -250,6 +253,31 @@ class Engine:
             a = int(acc[b])
             out.append((a, int(nxt[b]), nodes[b * k:b * k + a].copy() if parents is not None else None))
         return out
+
+    def verify_sample(self, seq: int, draft, eps, u, q=None, temperature: float = 1.0, residual: bool = True):
+        """Stochastic verification (Eq. 4).  ``q``: None (greedy draft) or a
+        [K, vocab] float32 array of draft distributions (uploaded to the
+        device here); ``eps`` (K) and ``u`` (K + 1) are uniform draws.
+        Returns (accept_len, next_token)."""
+        d, dp = _i32arr(draft)
+        k = len(d)
+        e = np.ascontiguousarray(np.asarray(eps, dtype=np.float32).reshape(-1))
+        uu = np.ascontiguousarray(np.asarray(u, dtype=np.float32).reshape(-1))
+        if len(e) != k or len(uu) != k + 1:
+            raise EEError(EE_EINVAL, "eps needs K values and u K + 1")
+        qdev = None
+        if q is not None:
+            qa = np.ascontiguousarray(np.asarray(q, dtype=np.float32))
+            if qa.shape != (k, self.shape.vocab):
+                raise EEError(EE_EINVAL, "q must be [K, vocab]")
+            qdev = torch.from_numpy(qa).to(self.device)
+            torch.cuda.synchronize(self.device)
+        a, nxt = ctypes.c_int32(), ctypes.c_int32()
+        _check(ee_verify_sample(self.ctx, seq, dp if k else None, k, qdev.data_ptr() if qdev is not None else None,
+                                e.ctypes.data_as(_pf32), uu.ctypes.data_as(_pf32), float(temperature),
+                                int(bool(residual)), ctypes.byref(a), ctypes.byref(nxt)), self.ctx)
+        self._last_rows = k + 1
+        return a.value, nxt.value
 
     def verify_topk(self, seqs, drafts, top_k: int, dynamic: bool = True):
         """Entropy-aware (``dynamic``) or fixed top-k verification of linear

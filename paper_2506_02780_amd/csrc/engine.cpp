@@ -43,9 +43,9 @@ struct Layout {
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
-  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, result, stage, rope, ws_total;
+  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, rowstat, ebuf, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
-  size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, stage_bytes;
+  size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, s_eps, s_unif, s_sparam, stage_bytes;
   size_t kv_layer, kv_total;
 };
 
@@ -135,6 +135,8 @@ Layout make_layout(const ee_model_config* c) {
   L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8 * 8);
   L.greedy = o; o += up(L.Rmax * 4);
   L.verdict = o; o += up(L.Rmax * 4);
+  L.rowstat = o; o += up((size_t)L.Rmax * 2 * 8);
+  L.ebuf = o; o += up((size_t)L.Rmax * V * 8);
   L.result = o; o += up((size_t)c->max_seqs * (2 + c->k_max) * 4);
   // staging block: one host->device copy per call
   size_t so = 0;
@@ -146,6 +148,10 @@ Layout make_layout(const ee_model_config* c) {
   so = (so + 15) & ~(size_t)15;   // 16-byte loads of page numbers
   L.s_ptable = so; so += (size_t)c->max_seqs * L.ptable_len * 4;
   L.s_info = so; so += (size_t)c->max_seqs * 4 * 4;
+  L.s_eps = so; so += (size_t)L.Rmax * 4;
+  L.s_unif = so; so += (size_t)L.Rmax * 4;
+  so = (so + 15) & ~(size_t)15;
+  L.s_sparam = so; so += 16;
   L.stage_bytes = up(so);
   L.stage = o; o += L.stage_bytes;
   L.rope = o; o += up((size_t)c->max_ctx * (hd / 2) * 8);
@@ -223,6 +229,8 @@ void bind_work(ee_ctx* c) {
   w.amax = reinterpret_cast<unsigned long long*>(ws + L.amax);
   w.greedy = reinterpret_cast<int*>(ws + L.greedy);
   w.verdict = reinterpret_cast<int*>(ws + L.verdict);
+  w.rowstat = reinterpret_cast<double*>(ws + L.rowstat);
+  w.ebuf = reinterpret_cast<double*>(ws + L.ebuf);
   w.result = reinterpret_cast<int*>(ws + L.result);
   unsigned char* sb = ws + L.stage;
   w.path = sb + L.s_path;
@@ -232,6 +240,9 @@ void bind_work(ee_ctx* c) {
   w.slot = reinterpret_cast<int*>(sb + L.s_slot);
   w.ptable = reinterpret_cast<int*>(sb + L.s_ptable);
   w.info = reinterpret_cast<int*>(sb + L.s_info);
+  w.eps = reinterpret_cast<float*>(sb + L.s_eps);
+  w.unif = reinterpret_cast<float*>(sb + L.s_unif);
+  w.sparam = sb + L.s_sparam;
   w.ptable_len = L.ptable_len;
   w.rec = 2 + c->cfg.k_max;
   w.max_splits = L.max_splits;
@@ -718,6 +729,55 @@ int32_t ee_verify_topk(ee_ctx* c, int32_t n_seq, const int32_t* seqs, const int3
   if (top_k < 1 || top_k > 8 || top_k > c->cfg.vocab) return fail(c, EE_EINVAL, "top_k outside [1, min(8, vocab)]");
   return verify_many(c, n_seq, seqs, drafts, K, nullptr, top_k, dynamic ? 1 : 0, accept_lens, next_tokens,
                      nullptr, thresholds);
+}
+
+int32_t ee_verify_sample(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const float* q_dev,
+                         const float* eps, const float* u, float temperature, int32_t residual,
+                         int32_t* accept_len, int32_t* next_token) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!accept_len || !next_token || !u || (K > 0 && !eps))
+    return fail(c, EE_EINVAL, "eps (K > 0), u, accept_len and next_token must be non-NULL");
+  Seq& s = c->seqs[seq];
+  if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
+  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
+  if (!(temperature > 0.f) || !(temperature < INFINITY)) return fail(c, EE_EINVAL, "temperature must be positive");
+  if (c->cfg.vocab > 4096 * 64) return fail(c, EE_EINVAL, "stochastic verification handles vocabularies up to 262144");
+  for (int i = 0; i < K; ++i)
+    if (!(eps[i] >= 0.f && eps[i] < 1.f)) return fail(c, EE_EINVAL, "eps outside [0, 1)");
+  for (int i = 0; i <= K; ++i)
+    if (!(u[i] >= 0.f && u[i] < 1.f)) return fail(c, EE_EINVAL, "u outside [0, 1)");
+  int depth[1];
+  if ((rc = check_draft(c, draft, K, nullptr, depth))) return rc;
+  const int T = K + 1;
+  if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
+  int added;
+  if (!reserve_pages(c, s, s.len + T, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  stage_draft(c, 0, T, s, draft, nullptr, depth);
+  const Layout& L = c->lay;
+  float* se = reinterpret_cast<float*>(c->h_stage + L.s_eps);
+  float* su = reinterpret_cast<float*>(c->h_stage + L.s_unif);
+  for (int i = 0; i < K; ++i) se[i] = eps[i];
+  for (int i = 0; i <= K; ++i) su[i] = u[i];
+  struct {
+    unsigned long long q;
+    float temperature;
+    int32_t residual;
+  } sp{(unsigned long long)(uintptr_t)q_dev, temperature, residual ? 1 : 0};
+  static_assert(sizeof(sp) == 16, "staged sampling parameters");
+  memcpy(c->h_stage + L.s_sparam, &sp, sizeof sp);
+  Seq* one = &s;
+  rc = run_block(c, &one, 1, T, 4);
+  if (rc) {
+    unreserve(c, s, added);
+    return rc;
+  }
+  const int a = c->h_result[0];
+  s.len += 1 + a;
+  s.pending = c->h_result[1];
+  *accept_len = a;
+  *next_token = s.pending;
+  return EE_OK;
 }
 
 int32_t ee_kv_rollback(ee_ctx* c, int32_t seq, int32_t new_len, int32_t pending_token) {

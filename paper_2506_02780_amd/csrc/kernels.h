@@ -69,7 +69,9 @@ struct Work {
   float* logits;            // [Rmax, V]
   unsigned long long* amax; // [Rmax, ceil(V/2048), 8] chunk maxima (top-8 in mode 3)
   int* greedy;              // [Rmax]
-  int* verdict;             // [Rmax] mode 3: tau | draft-accepted << 8
+  int* verdict;             // [Rmax] modes 3, 4: tau | draft-accepted << 8
+  double* rowstat;          // [Rmax][2] mode 4: row maximum and sum of exp((l - max) / temperature)
+  double* ebuf;             // [Rmax][V] mode 4: exp((l - max) / temperature) of every logit
   int* result;              // [max_seqs][rec]: accept_len, next, accepted rows (or thresholds)
   // staged per call (host -> device)
   int* tok;                 // [Rmax]
@@ -79,6 +81,9 @@ struct Work {
   unsigned char* path;      // [Rmax][64] tree mode (at most 64 nodes): entry j-1 of row t =
                             // block row at depth j on t's path (row 0, the pending token, is depth 0)
   int* ptable;              // [max_seqs][ptable_len] page of each 64-position block
+  float* eps;               // [Rmax] mode 4: acceptance draws of the draft rows
+  float* unif;              // [Rmax] mode 4: resampling draws (row a of the block)
+  const unsigned char* sparam;  // mode 4: {u64 draft distribution pointer or 0, f32 temperature, i32 residual}
   int* info;                // [max_seqs][4]: committed positions n, attention splits in use,
                             // top-k size k and dynamic flag (mode 3)
   int ptable_len;           // entries per sequence (multiple of 4)
@@ -104,7 +109,8 @@ struct Prof {
 struct Step {
   int T;        // rows per sequence
   int B;        // sequences in the block
-  int mode;     // 0 prefill, 1 linear verify, 2 tree verify, 3 linear top-k verify
+  int mode;     // 0 prefill, 1 linear verify, 2 tree verify, 3 linear top-k verify,
+                // 4 linear stochastic verify (one sequence)
 };
 
 enum ProfClass {

@@ -1404,6 +1404,190 @@ __global__ __launch_bounds__(64) void topk_select_kernel(const unsigned long lon
   }
 }
 
+// Stochastic verification (Eq. 4), step 1, one workgroup per row: the row's
+// maximum logit M (from the chunk maxima), e_v = exp((l_v - M) / temp) (kept
+// in ebuf[t] for the draw that may follow at this row) and S = sum_v e_v, in
+// float64 with a fixed summation order; draft row t (t + 1 < T) accepts token
+// d = tok[t + 1] when eps_t * q_t[d] < p_t[d] = e_d / S, with q_t[d] from the
+// draft distribution (1 when none is given: a greedy draft).  verdict[t] bit
+// 8 = accepted; greedy[t] = the row's argmax; rowstat[t] = (M, S).
+struct SampleParams {
+  unsigned long long q;   // device address of the draft distribution [K][V] fp32, or 0
+  float temperature;
+  int residual;
+};
+constexpr int SAMPLE_MAX_GROUPS = 4096;   // 64-token groups: vocabularies up to 262144 tokens
+
+__device__ __forceinline__ double sample_weight(const double* e, const float* q, int d, int v, double S, bool resid) {
+  if (!resid) return e[v];
+  const double p = e[v] / S;
+  const double qv = q ? (double)q[v] : (v == d ? 1.0 : 0.0);
+  return p > qv ? p - qv : 0.0;
+}
+
+__global__ __launch_bounds__(256) void sample_stats_kernel(const float* __restrict__ logits,
+                                                           const unsigned long long* __restrict__ amax, int nchunk,
+                                                           int V, const int* __restrict__ tok, int T,
+                                                           const float* __restrict__ eps,
+                                                           const unsigned char* __restrict__ sparam,
+                                                           double* __restrict__ rowstat, double* __restrict__ ebuf,
+                                                           int* __restrict__ greedy, int* __restrict__ verdict) {
+  __shared__ double sh[256];
+  __shared__ unsigned long long shk[256];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const SampleParams sp = *reinterpret_cast<const SampleParams*>(sparam);
+  unsigned long long best = 0;
+  for (int i = tid; i < nchunk; i += 256) best = amax[(size_t)t * nchunk + i] > best ? amax[(size_t)t * nchunk + i] : best;
+  shk[tid] = best;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w && shk[tid + w] > shk[tid]) shk[tid] = shk[tid + w];
+    __syncthreads();
+  }
+  const unsigned long long key = shk[0];
+  const double M = (double)key_value(key), it = 1.0 / (double)sp.temperature;
+  const float* row = logits + (size_t)t * V;
+  double* e = ebuf + (size_t)t * V;
+  double acc = 0.0;
+  for (int v = tid; v < V; v += 256) {
+    const double ev = exp(((double)row[v] - M) * it);
+    e[v] = ev;
+    acc += ev;
+  }
+  sh[tid] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) sh[tid] += sh[tid + w];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double S = sh[0];
+    rowstat[2 * t] = M;
+    rowstat[2 * t + 1] = S;
+    greedy[t] = key_index(key);
+    int ok = 0;
+    if (t + 1 < T) {
+      const int d = tok[t + 1];
+      const double pd = exp(((double)row[d] - M) * it) / S;
+      const double qd = sp.q ? (double)reinterpret_cast<const float*>(sp.q)[(size_t)t * V + d] : 1.0;
+      ok = (double)eps[t] * qd < pd ? 1 : 0;
+    }
+    verdict[t] = ok << 8;
+  }
+}
+
+// Stochastic verification, step 2 (after the acceptance scan), one workgroup:
+// row a = result[0] draws the next token by inverse CDF with u = unif[a] over
+// w_v = max(0, p_v - q_v) (a rejected draft row with `residual`; p instead
+// when the residual vanishes) or over e_v, proportional to p (the bonus row,
+// or no residual): the smallest v whose cumulative weight in token order
+// exceeds u times the total.  The vocabulary is cut into 64-token groups;
+// group sums (tiles of 64 groups transposed through LDS, each summed in token
+// order), runs of groups per thread, run offsets in thread order, then an
+// inclusive scan over the chosen group's tokens.  float64; rounding that
+// leaves the target past every sum picks the last token of non-zero weight.
+__global__ __launch_bounds__(256) void resample_kernel(const double* __restrict__ ebuf, int V, const int* __restrict__ tok,
+                                                       int T, const float* __restrict__ unif,
+                                                       const unsigned char* __restrict__ sparam,
+                                                       const double* __restrict__ rowstat, int* __restrict__ result) {
+  __shared__ double tile[64][65];
+  __shared__ double gs[SAMPLE_MAX_GROUPS];
+  __shared__ double run_s[256], run_o[257];
+  __shared__ int sel[2];
+  __shared__ double sel_off;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const SampleParams sp = *reinterpret_cast<const SampleParams*>(sparam);
+  const int a = result[0];
+  const int K = T - 1;
+  const double S = rowstat[2 * a + 1];
+  const double* e = ebuf + (size_t)a * V;
+  const bool draft_row = a < K;
+  const int d = draft_row ? tok[a + 1] : -1;
+  const float* q = (draft_row && sp.q) ? reinterpret_cast<const float*>(sp.q) + (size_t)a * V : nullptr;
+  bool resid = draft_row && sp.residual;
+  const int ng = (V + 63) / 64, per = (ng + 255) / 256;
+  const int r0 = min(ng, tid * per), r1 = min(ng, r0 + per);
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int base = 0; base < ng; base += 64) {
+      for (int k = tid; k < 64 * 64; k += 256) {
+        const int v = base * 64 + k;
+        tile[k >> 6][k & 63] = v < V ? sample_weight(e, q, d, v, S, resid) : 0.0;
+      }
+      __syncthreads();
+      if (tid < 64 && base + tid < ng) {
+        double sum = 0.0;
+        for (int j = 0; j < 64; ++j) sum += tile[tid][j];
+        gs[base + tid] = sum;
+      }
+      __syncthreads();
+    }
+    double run = 0.0;
+    for (int g = r0; g < r1; ++g) run += gs[g];
+    run_s[tid] = run;
+    __syncthreads();
+    if (tid == 0) {
+      double o = 0.0;
+      for (int i = 0; i < 256; ++i) {
+        run_o[i] = o;
+        o += run_s[i];
+      }
+      run_o[256] = o;
+    }
+    __syncthreads();
+    if (!(resid && !(run_o[256] > 0.0))) break;
+    resid = false;   // p == q: nothing to correct, draw from p
+    __syncthreads();
+  }
+  const double target = (double)unif[a] * run_o[256];
+  if (tid == 0) {
+    sel[0] = -1;
+    sel[1] = -1;
+  }
+  __syncthreads();
+  // the run, then the group, holding the target; else the last group of non-zero weight
+  if (r0 < r1 && target >= run_o[tid] && target < run_o[tid] + run_s[tid]) {
+    double c = run_o[tid];
+    for (int g = r0; g < r1; ++g) {
+      if (gs[g] > 0.0 && target < c + gs[g]) {
+        sel[0] = g;
+        sel_off = c;
+        break;
+      }
+      c += gs[g];
+    }
+  }
+  __syncthreads();
+  if (tid == 0 && sel[0] < 0) {
+    double c = 0.0;
+    for (int g = 0; g < ng; ++g) {
+      if (gs[g] > 0.0) {
+        sel[0] = g;
+        sel_off = c;
+      }
+      c += gs[g];
+    }
+    if (sel[0] < 0) sel[0] = 0;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    const int g = sel[0];
+    const int v = g * 64 + lane;
+    const double wv = v < V ? sample_weight(e, q, d, v, S, resid) : 0.0;
+    double incl = wv;   // inclusive scan over the group in token order
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const double y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    const unsigned long long over = __ballot(wv > 0.0 && sel_off + incl > target);
+    const unsigned long long pos = __ballot(wv > 0.0);
+    int chosen;
+    if (over) chosen = g * 64 + (__ffsll((long long)over) - 1);
+    else chosen = pos ? g * 64 + (63 - __clzll((long long)pos)) : g * 64;
+    if (lane == 0) result[1] = chosen;
+  }
+}
+
 // result[0] = accepted rows a, result[1] = next token, result[2..2+a) = accepted
 // block rows in depth order (mode 3: result[2..2+K) = the threshold tau of
 // every draft row).  Mode 0 (prefill) commits every row.
@@ -1427,10 +1611,11 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
     }
     return;
   }
-  if (mode == 1 || mode == 3) {
+  if (mode == 1 || mode == 3 || mode == 4) {
     // draft d_{i+1} (row i+1) is checked against row i: its greedy token
-    // (mode 1) or its top-k verdict (mode 3); the first failing row, found 64
-    // rows at a time, is a.  Mode 3 also records every row's threshold.
+    // (mode 1) or its verdict (mode 3: top-k, mode 4: stochastic); the first
+    // failing row, found 64 rows at a time, is a.  Mode 3 also records every
+    // row's threshold.
     int a = K;
     for (int i0 = 0; i0 < K; i0 += 64) {
       const int i = i0 + lane;
@@ -1438,6 +1623,8 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
       if (i < K) {
         if (mode == 1) {
           fails = tok[i + 1] != greedy[i];
+        } else if (mode == 4) {
+          fails = !((verdict[i] >> 8) & 1);
         } else {
           const int vd = verdict[i];
           fails = !((vd >> 8) & 1);
@@ -1446,13 +1633,13 @@ __global__ __launch_bounds__(64) void accept_kernel(const int* __restrict__ tok,
       }
       const unsigned long long b = __ballot(fails);
       if (b && a == K) a = i0 + __ffsll((long long)b) - 1;
-      if (mode == 1 && a != K) break;
+      if (mode != 3 && a != K) break;
     }
     if (lane == 0) {
       result[0] = a;
       result[1] = greedy[a];
     }
-    if (mode == 1)
+    if (mode != 3)
       for (int i = lane; i < a; i += 64) result[2 + i] = i + 1;
     return;
   }
@@ -1655,6 +1842,9 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if (topk)
       hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(64), 0, st, w.amax, nchunk, w.tok, w.info, s.T,
                          w.greedy, w.verdict);
+    else if (s.mode == 4)
+      hipLaunchKernelGGL(sample_stats_kernel, dim3(R), dim3(256), 0, st, w.logits, w.amax, nchunk, m.V, w.tok, s.T,
+                         w.eps, w.sparam, w.rowstat, w.ebuf, w.greedy, w.verdict);
     else
       hipLaunchKernelGGL(argmax_kernel, dim3(R), dim3(256), 0, st, w.amax, nchunk, w.greedy);
     return last();
@@ -1669,10 +1859,12 @@ hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof,
 }
 
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
-  (void)m;
   return timed(prof, PC_ACCEPT, st, [&] {
     hipLaunchKernelGGL(accept_kernel, dim3(s.B), dim3(64), 0, st, w.tok, w.prow, w.greedy, w.verdict, s.T,
                        s.mode, w.result, w.rec);
+    if (s.mode == 4)   // one sequence: draw the next token at the accepted length
+      hipLaunchKernelGGL(resample_kernel, dim3(1), dim3(256), 0, st, w.ebuf, m.V, w.tok, s.T, w.unif, w.sparam,
+                         w.rowstat, w.result);
     return hipGetLastError();
   });
 }
