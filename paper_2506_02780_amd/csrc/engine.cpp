@@ -77,6 +77,16 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
     const size_t layer = pages * 2 * c->n_kv_heads * PAGE * c->head_dim * (c->dtype == EE_BF16 ? 2 : 4);
     if (layer >= (size_t(1) << 31)) return bad("one layer of the KV pool must stay below 2 GiB");
   }
+  {
+    // GEMM slice partials of one block are written through 32-bit buffer offsets
+    const int dt = c->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
+    const size_t rows = (size_t)(c->k_max + 1) * c->max_seqs;
+    const size_t n_max = std::max({(size_t)c->vocab, (size_t)2 * c->ffn,
+                                   (size_t)(c->n_heads + 2 * c->n_kv_heads) * c->head_dim});
+    const size_t sk = (size_t)std::max(ee::gemm_slices_for(c->d_model, dt), ee::gemm_slices_for(c->ffn, dt));
+    if (sk * rows * n_max * 4 >= (size_t(1) << 31))
+      return bad("the GEMM partials of one block must stay below 2 GiB (fewer sequences or draft tokens)");
+  }
   return true;
 }
 

@@ -205,6 +205,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
   const int S = a.S, s0 = k * a.SS, ns = min(S - s0, a.SS);
   const auto xs = make_rsrc(a.x + (size_t)(row0 / 16) * S * 64, (unsigned)(MT * S * 1024));
   const auto ws = make_rsrc(a.w, (unsigned)((size_t)a.n_tiles * S * 1024));
+  const auto ps = make_rsrc(a.part, (unsigned)((size_t)a.SK * a.Ttot * a.N * 4));
   constexpr int WAUX = NT ? 2 : 0;
   uint4 xr[GEMM_SPW][MT];
 #pragma unroll
@@ -215,44 +216,53 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
       xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < T)
                                   ? (unsigned)(((m * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
-  __shared__ f32x4 red[2][GEMM_WAVES][MT][64];
-  uint4 wr[GEMM_SPW];
-  int tile = q / a.SK;
-#pragma unroll
-  for (int i = 0; i < GEMM_SPW; ++i) {
+  auto wload = [&](int tl, int i) {
     const int sl = wv + GEMM_WAVES * i;
-    wr[i] = bload<WAUX>(ws, (tile < a.n_tiles && sl < ns)
-                                ? (unsigned)(((tile * S + s0 + sl) * 64 + lane) * 16) : OOB);
-  }
-  for (int it = 0; tile < a.n_tiles; tile += groups, ++it) {
-    const int tn = tile + groups;
+    return bload<WAUX>(ws, (tl < a.n_tiles && sl < ns) ? (unsigned)(((tl * S + s0 + sl) * 64 + lane) * 16) : OOB);
+  };
+  __shared__ f32x4 red[2][GEMM_WAVES][MT][64];
+  // this thread's reduction item: fragment rm, lane rl (threads past MT * 64
+  // repeat an item and store nothing: the loop body has no branch, so the
+  // compiler never has to wait for the weights in flight at the loop edge)
+  const int qq = threadIdx.x % (MT * 64);
+  const bool qown = threadIdx.x < MT * 64;
+  const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
+  auto tile_step = [&](const uint4 (&wf)[GEMM_SPW], int tile, int pb) {
     f32x4 acc[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < GEMM_SPW; ++i) {
-      const uint4 wf = wr[i];
-      const int sl = wv + GEMM_WAVES * i;
-      wr[i] = bload<WAUX>(ws, (tn < a.n_tiles && sl < ns)
-                                  ? (unsigned)(((tn * S + s0 + sl) * 64 + lane) * 16) : OOB);
+    for (int i = 0; i < GEMM_SPW; ++i)
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[m] = mma<DT>(wf, xr[i][m], acc[m]);
-    }
-    const int pb = it & 1;   // two reduction buffers: one barrier per tile
+      for (int m = 0; m < MT; ++m) acc[m] = mma<DT>(wf[i], xr[i][m], acc[m]);
 #pragma unroll
     for (int m = 0; m < MT; ++m) red[pb][wv][m][lane] = acc[m];
     __syncthreads();
-    for (int qq = threadIdx.x; qq < MT * 64; qq += GEMM_WAVES * 64) {
-      const int m = qq >> 6, ln = qq & 63;
-      f32x4 v = red[pb][0][m][ln];
+    f32x4 v = red[pb][0][rm][rl];
 #pragma unroll
-      for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][m][ln];
-      const int t = m * 16 + (ln & 15);
-      if (t < T) {
-        float* o = a.part + ((size_t)k * a.Ttot + row0 + t) * a.N + tile * 16 + 4 * (ln >> 4);
-        *reinterpret_cast<float4*>(o) = make_float4(v.x, v.y, v.z, v.w);
-      }
-    }
+    for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][rm][rl];
+    const unsigned off = (qown && rt < T)
+        ? (unsigned)((((size_t)k * a.Ttot + row0 + rt) * a.N + tile * 16 + 4 * (rl >> 4)) * 4) : OOB;
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y),
+                                                 __float_as_uint(v.z), __float_as_uint(v.w)}, ps, off, 0, 0);
+  };
+  // two named weight buffers: the next tile's fragments are requested before
+  // the current tile is computed, and no in-flight register is ever copied
+  int tile = q / a.SK;
+  uint4 wa[GEMM_SPW], wb[GEMM_SPW];
+#pragma unroll
+  for (int i = 0; i < GEMM_SPW; ++i) wa[i] = wload(tile, i);
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < GEMM_SPW; ++i) wb[i] = wload(tile + groups, i);
+    tile_step(wa, tile, 0);
+    tile += groups;
+    if (tile >= a.n_tiles) break;
+#pragma unroll
+    for (int i = 0; i < GEMM_SPW; ++i) wa[i] = wload(tile + groups, i);
+    tile_step(wb, tile, 1);
+    tile += groups;
+    if (tile >= a.n_tiles) break;
   }
 }
 
@@ -624,7 +634,7 @@ template <int DT, int HD, int THREADS> struct AttnLds {
   static constexpr int ROWB = HD * ESZ, KROW = ROWB + 16, VROW = 64 * ESZ + 16;
   static constexpr int KSUB = 64 * KROW, VSUB = HD * VROW;
   static constexpr int KV_BYTES = NSUB * (KSUB + VSUB);
-  static constexpr int ST_BYTES = (THREADS / 64) * (HD * 17 + 32) * 4;   // merge states
+  static constexpr int ST_BYTES = (THREADS / 64) * (16 * (HD + 4) + 32) * 4;   // merge states
   static constexpr int BYTES = KV_BYTES > ST_BYTES ? KV_BYTES : ST_BYTES;
   static constexpr int UNITS = 2 * 64 * HD * ESZ / 16;             // uint4 per sub-tile (K + V)
   static constexpr int PER = (NSUB * UNITS + THREADS - 1) / THREADS;
@@ -1084,15 +1094,16 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   // gather sub-tile's slot is filled row by row by the waves that computed
   // the rows.
   __syncthreads();
-  float* stO = reinterpret_cast<float*>(lds);                          // [ATT_QT][NSUB][HD][17]
-  float* stM = stO + ATT_QT * NSUB * HD * 17;                           // [ATT_QT][NSUB][16]
+  // state rows [column][HD + 4] floats: a lane's four dims 16dt + 4grp .. +3
+  // are one 16-byte chunk (rows padded by 16 bytes: conflict-free)
+  constexpr int SROW = HD + 4;
+  float* stO = reinterpret_cast<float*>(lds);                          // [ATT_QT][NSUB][16][SROW]
+  float* stM = stO + ATT_QT * NSUB * 16 * SROW;                         // [ATT_QT][NSUB][16]
   float* stL = stM + ATT_QT * NSUB * 16;
   auto put_state = [&](int slot, const f32x4 (&ov)[ND], float mv, float lv) {
-  float* so = stO + ((size_t)(qi * NSUB + slot) * HD) * 17;
+  float* so = stO + ((size_t)(qi * NSUB + slot) * 16 + c) * SROW;
 #pragma unroll
-  for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) so[(16 * dt + 4 * grp + r) * 17 + c] = ov[dt][r];
+  for (int dt = 0; dt < ND; ++dt) *reinterpret_cast<f32x4*>(so + 16 * dt + 4 * grp) = ov[dt];
   if (grp == 0) {
     stM[(qi * NSUB + slot) * 16 + c] = mv;
     stL[(qi * NSUB + slot) * 16 + c] = lv;
@@ -1129,9 +1140,12 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   if (!(lj > 0.f)) continue;
   const float w = exp2f(stM[(mq * NSUB + j) * 16 + col] - M);
   L = fmaf(lj, w, L);
-  const float* so = stO + ((size_t)(mq * NSUB + j) * HD + d0) * 17 + col;
+  const float* so = stO + ((size_t)(mq * NSUB + j) * 16 + col) * SROW + d0;
+  float sv[DPT];
 #pragma unroll
-  for (int e = 0; e < DPT; ++e) O[e] = fmaf(so[e * 17], w, O[e]);
+  for (int e = 0; e < DPT; e += 4) *reinterpret_cast<f32x4*>(sv + e) = *reinterpret_cast<const f32x4*>(so + e);
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) O[e] = fmaf(sv[e], w, O[e]);
   }
   float* out = a.part + (((size_t)sp * a.Hkv + gkv) * ((size_t)a.B * a.ncols) + (size_t)b * a.ncols + qcol) * (HD + 2);
 #pragma unroll
