@@ -339,6 +339,166 @@ __device__ __forceinline__ void store8(void* xout, int t, int col, int S, const 
   }
 }
 
+// ------------------------------------------------------ gate/up + SwiGLU --
+//
+// For reductions of at most FK_MAX_S super-steps (d <= 4096 in bf16) the
+// gate/up projection runs without K slices and applies SwiGLU itself:
+//   * a workgroup owns pairs of tiles (gate features 16p .. 16p+15 and the up
+//     features with the same indices) and reduces each over the whole of K:
+//     wave w accumulates super-steps w, w+8, w+16, ... in order, the 8 wave
+//     sums are added in wave order;
+//   * its rows: up to 33, rows 0..31 as two register tiles and the 33rd from
+//     LDS (one fragment column per super-step); blocks of more rows run as
+//     32-row groups of one launch (the last group may hold 33), and with P a
+//     multiple of 8 the groups that stream the same weights share an XCD;
+//   * z = silu(gate) * up goes straight into the down projection's packed
+//     activations: no slice partials, no separate SwiGLU launch.
+// A row's arithmetic depends only on K, never on the block's rows.
+
+constexpr int FK_MAX_S = 128;   // super-steps one workgroup reduces (16 per wave)
+constexpr int FK_GROUP = 32;    // rows of a group held in registers
+
+__host__ __device__ inline int fk_groups(int R) { return R <= FK_GROUP + 1 ? 1 : (R - 1 + FK_GROUP - 1) / FK_GROUP; }
+
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
+
+struct FkArgs {
+  const uint4* w;   // packed [2F, d]: gate rows, then up rows
+  const uint4* x;   // packed activations of all R rows
+  void* z;          // packed [R, F] activations of the down projection
+  int S, n_pairs;   // super-steps of d; F / 16
+  int R, P, z_S;    // rows; workgroups per row group; super-steps of F
+};
+
+template <int DT, int MTV, int SPW>
+__global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, c = lane & 15, grp = lane >> 4;
+  const int rg = blockIdx.x / a.P, g = blockIdx.x - rg * a.P;
+  const int ngroups = fk_groups(a.R);
+  const int row0 = rg * FK_GROUP;
+  const int T = rg == ngroups - 1 ? a.R - row0 : FK_GROUP;   // rows of this group, <= 33
+  const bool rowl = MTV == 2 && T > 2 * 16;                  // the 33rd row, from LDS
+  const int S = a.S;
+  constexpr int NR = MTV == 2 ? 3 : 1;                       // reduced fragment tiles
+  constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
+  const auto xs = make_rsrc(a.x, (unsigned)((size_t)((a.R + 15) / 16) * S * 1024));
+  const auto ws = make_rsrc(a.w, (unsigned)((size_t)2 * a.n_pairs * S * 1024));
+  __shared__ uint4 rowx[MTV == 2 ? FK_MAX_S * 4 : 1];        // [super-step][grp]: the 33rd row
+  __shared__ f32x4 red[2][GEMM_WAVES][NR][64];
+  uint4 xr[SPW][MTV];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int sl = wv + GEMM_WAVES * i;
+#pragma unroll
+    for (int m = 0; m < MTV; ++m)
+      xr[i][m] = bload<0>(xs, (sl < S && m * 16 + c < min(T, 2 * 16))
+                                  ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
+  }
+  if (MTV == 2) {
+    for (int it = threadIdx.x; it < S * 4; it += GEMM_WAVES * 64)
+      rowx[it] = bload<0>(xs, rowl ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
+                                   : OOB);
+  }
+  // tile k of this workgroup: pair g + (k / 2) P, gate (k even) or up (k odd)
+  const int npair = g < a.n_pairs ? (a.n_pairs - g + a.P - 1) / a.P : 0;
+  const int ntile = 2 * npair;
+  auto tile_of = [&](int k) { return g + (k >> 1) * a.P + (k & 1) * a.n_pairs; };
+  auto wload = [&](int k, int i) {
+    const int sl = wv + GEMM_WAVES * i;
+    return bload<2>(ws, (k < ntile && sl < S) ? (unsigned)(((tile_of(k) * S + sl) * 64 + lane) * 16) : OOB);
+  };
+  __syncthreads();
+  // this thread's reduced item: fragment tile rm, lane rl (threads past NR * 64
+  // repeat an item and store nothing)
+  const int qq = threadIdx.x % (NR * 64);
+  const bool qown = threadIdx.x < NR * 64;
+  const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
+  f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 wa[HA], wb[HB > 0 ? HB : 1];
+#pragma unroll
+  for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
+  for (int k = 0; k < ntile; ++k) {
+    f32x4 acc[NR];
+#pragma unroll
+    for (int m = 0; m < NR; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto step = [&](const uint4& wf, int i) {
+#pragma unroll
+      for (int m = 0; m < MTV; ++m) acc[m] = mma<DT>(wf, xr[i][m], acc[m]);
+      if (MTV == 2) {
+        const uint4 r = rowx[(wv + GEMM_WAVES * i) * 4 + grp];
+        acc[2] = mma<DT>(wf, c == 0 ? r : make_uint4(0u, 0u, 0u, 0u), acc[2]);
+      }
+    };
+    // second half of this tile in flight while the first is multiplied, then
+    // the first half of the next tile while the second is
+#pragma unroll
+    for (int i = 0; i < HB; ++i) wb[i] = wload(k, HA + i);
+#pragma unroll
+    for (int i = 0; i < HA; ++i) step(wa[i], i);
+#pragma unroll
+    for (int i = 0; i < HA; ++i) wa[i] = wload(k + 1, i);
+#pragma unroll
+    for (int i = 0; i < HB; ++i) step(wb[i], HA + i);
+    const int pb = k & 1;
+#pragma unroll
+    for (int m = 0; m < NR; ++m) red[pb][wv][m][lane] = acc[m];
+    __syncthreads();
+    f32x4 v = red[pb][0][rm][rl];
+#pragma unroll
+    for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][rm][rl];
+    if (!(k & 1)) {
+      gate = v;
+    } else if (qown && rt < T) {
+      // features 16p + 4(rl / 16) .. +3 of row row0 + rt
+      const int f = 16 * (g + (k >> 1) * a.P) + 4 * (rl >> 4);
+      float zv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) zv[r] = silu_mul(gate[r], v[r]);
+      const size_t fi = frag_index<DT>(row0 + rt, f, a.z_S);
+      if (DT == DT_BF16) {
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.z) + fi) =
+            make_uint2(f2bf_bits(zv[0]) | (f2bf_bits(zv[1]) << 16), f2bf_bits(zv[2]) | (f2bf_bits(zv[3]) << 16));
+      } else {
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.z) + fi) = make_float4(zv[0], zv[1], zv[2], zv[3]);
+      }
+    }
+  }
+}
+
+template <int DT, int MTV>
+static void launch_gemm_swiglu(const FkArgs& a, int spw, dim3 grid, hipStream_t st) {
+  const dim3 block(GEMM_WAVES * 64);
+  switch (spw) {
+    case 1: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 2>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 4>), grid, block, 0, st, a); break;
+    case 8: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 8>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 16>), grid, block, 0, st, a); break;
+  }
+}
+
+// z = silu(x Wg^T) * (x Wu^T) for R rows, when d / KS <= FK_MAX_S.
+template <int DT>
+static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, int R, void* z, hipStream_t st) {
+  FkArgs a;
+  a.w = wgu; a.x = x; a.z = z;
+  a.S = d / Geo<DT>::KS;
+  a.n_pairs = F / 16;
+  a.R = R;
+  a.z_S = F / Geo<DT>::KS;
+  if (a.S > FK_MAX_S || F % 16) return hipErrorInvalidValue;
+  int spw = 1;
+  while (spw * GEMM_WAVES < a.S) spw *= 2;
+  const int ng = fk_groups(R);
+  a.P = ng == 1 ? std::max(1, std::min(256, a.n_pairs)) : std::max(8, 256 / ng / 8 * 8);
+  const dim3 grid(ng * a.P);
+  if (R <= 16) launch_gemm_swiglu<DT, 1>(a, spw, grid, st);
+  else launch_gemm_swiglu<DT, 2>(a, spw, grid, st);
+  return hipGetLastError();
+}
+
+inline bool fused_swiglu(int d, int dt) { return d / ks_of(dt) <= FK_MAX_S; }
+
 // ------------------------------------------------------------ embed / norm --
 
 constexpr int NORM_THREADS = 512;
@@ -489,7 +649,7 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ p
   const float u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
   float z[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) z[e] = g[e] / (1.0f + expf(-g[e])) * u[e];
+  for (int e = 0; e < 8; ++e) z[e] = silu_mul(g[e], u[e]);
   store8<DT>(zout, t, f, z_S, z);
 }
 
@@ -1817,15 +1977,24 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            return last();
          })) != hipSuccess)
       return e;
-    // gate/up projection, then SwiGLU
-    if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st); })) != hipSuccess)
-      return e;
-    if ((e = timed(prof, PC_FINISH, st, [&] {
-           hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, R), dim3(256), 0, st, w.part, sk_d,
-                              R, m.F, (void*)w.zbuf, Sf);
-           return last();
-         })) != hipSuccess)
-      return e;
+    // gate/up projection and SwiGLU: fused for d / KS <= FK_MAX_S, else
+    // split-K partials and a SwiGLU launch
+    if (fused_swiglu(d, DT)) {
+      if ((e = timed(prof, PC_GATEUP, st, [&] {
+             return gemm_swiglu<DT>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st);
+           })) != hipSuccess)
+        return e;
+    } else {
+      if ((e = timed(prof, PC_GATEUP, st, [&] { return gemm<DT>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st); })) !=
+          hipSuccess)
+        return e;
+      if ((e = timed(prof, PC_FINISH, st, [&] {
+             hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, R), dim3(256), 0, st, w.part, sk_d,
+                                R, m.F, (void*)w.zbuf, Sf);
+             return last();
+           })) != hipSuccess)
+        return e;
+    }
     // down projection; residual add + the next norm (layer l+1 attention side, or final)
     if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT>(lp.wd, w.zbuf, d, m.F, R, w.part, st); })) != hipSuccess)
       return e;
@@ -1894,8 +2063,14 @@ hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hi
                           : gemm<DT_F32>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st); break;
       case PC_OPROJ: e = bf ? gemm<DT_BF16>(lp.wo, w.xbuf, d, qdim, R, w.part, st)
                             : gemm<DT_F32>(lp.wo, w.xbuf, d, qdim, R, w.part, st); break;
-      case PC_GATEUP: e = bf ? gemm<DT_BF16>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st)
-                             : gemm<DT_F32>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st); break;
+      case PC_GATEUP:
+        if (fused_swiglu(d, m.dt))
+          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st)
+                 : gemm_swiglu<DT_F32>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st);
+        else
+          e = bf ? gemm<DT_BF16>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st)
+                 : gemm<DT_F32>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st);
+        break;
       case PC_DOWN: e = bf ? gemm<DT_BF16>(lp.wd, w.zbuf, d, m.F, R, w.part, st)
                            : gemm<DT_F32>(lp.wd, w.zbuf, d, m.F, R, w.part, st); break;
       default: break;
