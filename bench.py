@@ -59,31 +59,33 @@ def step_bytes(s, t: int, n: int) -> dict:
 
 
 def gateup_bytes(s, t: int) -> int:
-    """Algorithmic bytes of one gate/up GEMM launch: the [2F, d] weights and
-    the T normalised input rows it multiplies."""
+    """Algorithmic bytes of one fused gate/up + SwiGLU launch: the [2F, d]
+    weights, the T normalised input rows it multiplies and the T x F SwiGLU
+    outputs it writes."""
     esz = 2 if s.dtype == "bf16" else 4
-    return esz * (2 * s.ffn * s.d_model + t * s.d_model)
+    return esz * (2 * s.ffn * s.d_model + t * s.d_model + t * s.ffn)
 
 
 def _gemm_source_digest(path):
-    """sha256 of the GEMM section of the kernel source (from its section
-    banner to the next one): the code the counter figures were taken on."""
+    """sha256 of the fused gate/up + SwiGLU section of the kernel source (from
+    its section banner to the next one): the code the counter figures were
+    taken on."""
     import hashlib
     out, on = [], False
     for ln in open(path).read().splitlines(keepends=True):
         if ln.startswith("// ----"):
             if on:
                 break
-            on = ln.rstrip().endswith(" GEMM --")
+            on = ln.rstrip().endswith(" gate/up + SwiGLU --")
         if on:
             out.append(ln)
     return hashlib.sha256("".join(out).encode()).hexdigest() if out else None
 
 
 def measured_traffic():
-    """Per-launch HBM bytes of the gate/up GEMM from the committed counter
-    summary, or None if the GEMM source has changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "gemm_gateup_7b_k32_traffic.md")
+    """Per-launch HBM bytes of the gate/up kernel from the committed counter
+    summary, or None if its source has changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "gemm_swiglu_gateup_7b_k32_traffic.md")
     src = os.path.join(ROOT, "paper_2506_02780_amd", "csrc", "kernels.hip")
     try:
         text = open(path).read()
@@ -506,7 +508,7 @@ def main():
         "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4)},
         "roofline": {
-            "kernel": f"gemm_kernel<{shape.dtype}, MT={(T + 15) // 16}> (gate/up projection, T={T})",
+            "kernel": f"gemm_swiglu_kernel<{shape.dtype}> (gate/up projection + SwiGLU, T={T})",
             "measured": ("HIP events around 5 x 32 gate/up launches (every layer's weights in turn) run back "
                          "to back on the library stream after the timed steps, with the timed block's shape"),
             "bound": "hbm",

@@ -383,7 +383,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
   const auto xs = make_rsrc(a.x, (unsigned)((size_t)((a.R + 15) / 16) * S * 1024));
   const auto ws = make_rsrc(a.w, (unsigned)((size_t)2 * a.n_pairs * S * 1024));
-  __shared__ uint4 rowx[MTV == 2 ? FK_MAX_S * 4 : 1];        // [super-step][grp]: the 33rd row
+  __shared__ uint4 rowx[MTV == 2 ? SPW * GEMM_WAVES * 4 : 1];   // [super-step][grp]: the 33rd row
   __shared__ f32x4 red[2][GEMM_WAVES][NR][64];
   uint4 xr[SPW][MTV];
 #pragma unroll
@@ -395,9 +395,11 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
                                   ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
   }
   if (MTV == 2) {
-    for (int it = threadIdx.x; it < S * 4; it += GEMM_WAVES * 64)
-      rowx[it] = bload<0>(xs, rowl ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
-                                   : OOB);
+    // every entry the MFMAs read is written: zeros past K or without a 33rd row
+    for (int it = threadIdx.x; it < SPW * GEMM_WAVES * 4; it += GEMM_WAVES * 64)
+      rowx[it] = bload<0>(xs, (rowl && (it >> 2) < S)
+                                  ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
+                                  : OOB);
   }
   // tile k of this workgroup: pair g + (k / 2) P, gate (k even) or up (k odd)
   const int npair = g < a.n_pairs ? (a.n_pairs - g + a.P - 1) / a.P : 0;
