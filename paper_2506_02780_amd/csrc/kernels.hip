@@ -1435,15 +1435,19 @@ constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 // state of every split the grid may have written (max_splits, fixed at launch)
 // is fetched in one batch; only the first info[1] take part.
 template <int DT, int HD>
-__global__ __launch_bounds__(HD / 4) void attn_combine_kernel(const float* __restrict__ part,
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
                                                               const int* __restrict__ info, int max_splits,
                                                               int Hkv, int G, int ncols, int H, int T,
                                                               void* __restrict__ xout, int x_S) {
   // ncols: query columns of the whole block (all sequences); row t belongs to
   // sequence t / T
-  const int t = blockIdx.x / H, j = blockIdx.x % H;
+  // 1024 / HD (row, head) columns per workgroup, HD / 4 threads of 4 dims each
+  constexpr int TPC = HD / 4;
+  const int pq = blockIdx.x * (256 / TPC) + threadIdx.x / TPC;
+  if (pq >= ncols / G * H) return;
+  const int t = pq / H, j = pq % H;
   const int gkv = j / G, qc = t * G + (j % G);
-  const int dim = threadIdx.x * 4;
+  const int dim = (threadIdx.x % TPC) * 4;
   float ms[MAX_SPLITS], ls[MAX_SPLITS];
   float4 os[MAX_SPLITS];
   // vector (buffer) loads throughout: the (m, l) addresses are uniform, and
@@ -1965,7 +1969,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
-           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3(R * m.H), dim3(HD / 4), 0, st, w.attn_part,
+           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3((R * m.H + 1024 / HD - 1) / (1024 / HD)), dim3(256), 0,
+                              st, w.attn_part,
                               w.info, w.max_splits, m.Hkv, G, R * G, m.H, T, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
