@@ -111,3 +111,24 @@ def test_bf16_prefill_longer_than_block_matches_oracle(ee):
     np.testing.assert_allclose(lg, ref.last_logits[-len(lg):], rtol=0, atol=2e-2)
     assert p == q or float(np.sort(ref.last_logits[-1])[-1] - np.sort(ref.last_logits[-1])[-2]) <= 2e-2
     eng.close()
+
+
+def test_bf16_width_not_a_multiple_of_256_matches_oracle(ee):
+    """d = 1280: 40 super-steps of 32 columns, not a multiple of the 8 waves
+    that split a projection's reduction, so part of every wave's register and
+    LDS fragments lie past K.  Drafts of 64 tokens make 65-row blocks (two row
+    groups, the second with a 33rd row held in LDS); GQA with 5 query heads per
+    KV head."""
+    shape = _bf16_small(n_layers=1, d_model=1280, n_heads=10, n_kv_heads=2, ffn=2560)
+    w = gen_weights(shape, seed=31, gains="random")
+    code = zipf_tokens(shape.vocab, 400, seed=12)
+    ref, log = oracle_reuse_session(shape, w, code[:150], code, steps=3, k=64)
+    eng, pinned = _replay(ee, shape, w, code[:150], log, max_ctx=512, k=64, tol=2e-2)
+    assert pinned >= 1
+    k, v = eng.read_kv(0, 0)
+    rk, rv = ref.cache[0]
+    n = min(len(k), len(rk))
+    for got, want in ((k, rk), (v, rv)):
+        gg = to_f64(got[:n], "bf16")
+        assert np.abs(gg - want[:n]).max() <= 2e-2 * max(1.0, np.abs(want).max())
+    eng.close()
