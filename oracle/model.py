@@ -24,10 +24,16 @@ decoder-only code LLMs; its text does not spell the layers out):
     logits = (RMSNorm(h) * g_final) Wlm^T
 
 Everything is float64.  For bf16 models, the quantities a bf16 pipeline
-stores in bf16 are rounded to bf16 (nearest-even): the three norm outputs,
-q and k after RoPE, v (so the cache holds bf16 keys and values), the
-attention output o and the SwiGLU product.  Residual stream, scores,
-softmax and logits stay float64.  fp32 models are not rounded at all.
+stores in bf16 are rounded to bf16 (nearest-even): the inputs of the
+projections that follow a norm, q and k after RoPE, v (so the cache holds
+bf16 keys and values), the attention output o and the SwiGLU product.
+Residual stream, scores, softmax and logits stay float64.  fp32 models are
+not rounded at all.
+
+A norm followed by a projection, RMSNorm(h) * g W^T, is evaluated as
+r * ((h * g) W^T) with the row's scale r = 1 / sqrt(mean(h^2) + eps): the
+same value, with h * g as the quantity that is stored (and so rounded) before
+the projection.
 """
 
 from __future__ import annotations
@@ -43,6 +49,11 @@ def _rounder(dtype: str):
 
 def rmsnorm(h, gain, eps):
     return h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps) * gain
+
+
+def norm_scale(h, eps):
+    """The RMSNorm scale of every row of h: 1 / sqrt(mean(h^2) + eps), shape [T, 1]."""
+    return 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
 
 
 def rope(u, pos, theta):
@@ -136,10 +147,11 @@ def forward_block(shape, weights, cache, tokens, depth, vis):
     block_kv = []
     for l in range(shape.n_layers):
         lw = weights.layer(l)
-        x = rnd(rmsnorm(h, lw["attn_gain"].astype(np.float64), shape.rms_eps))
-        q = (x @ to_f64(lw["wq"], dt).T).reshape(t, H, hd)
-        k = (x @ to_f64(lw["wk"], dt).T).reshape(t, Hkv, hd)
-        v = (x @ to_f64(lw["wv"], dt).T).reshape(t, Hkv, hd)
+        x = rnd(h * lw["attn_gain"].astype(np.float64))      # RMSNorm(h) * g = r * (h * g)
+        r = norm_scale(h, shape.rms_eps)
+        q = ((x @ to_f64(lw["wq"], dt).T) * r).reshape(t, H, hd)
+        k = ((x @ to_f64(lw["wk"], dt).T) * r).reshape(t, Hkv, hd)
+        v = ((x @ to_f64(lw["wv"], dt).T) * r).reshape(t, Hkv, hd)
         q = rnd(rope(q, pos, shape.rope_theta))
         k = rnd(rope(k, pos, shape.rope_theta))
         v = rnd(v)
@@ -149,9 +161,10 @@ def forward_block(shape, weights, cache, tokens, depth, vis):
         vals = np.concatenate([vc, v], axis=0)
         o = rnd(attention(q, keys, vals, mask, scale).reshape(t, H * hd))
         h = h + o @ to_f64(lw["wo"], dt).T
-        x = rnd(rmsnorm(h, lw["ffn_gain"].astype(np.float64), shape.rms_eps))
-        z = rnd(silu(x @ to_f64(lw["w_gate"], dt).T) * (x @ to_f64(lw["w_up"], dt).T))
+        x = rnd(h * lw["ffn_gain"].astype(np.float64))
+        r = norm_scale(h, shape.rms_eps)
+        z = rnd(silu((x @ to_f64(lw["w_gate"], dt).T) * r) * ((x @ to_f64(lw["w_up"], dt).T) * r))
         h = h + z @ to_f64(lw["w_down"], dt).T
-    f = rnd(rmsnorm(h, weights.final_gain.astype(np.float64), shape.rms_eps))
-    logits = f @ to_f64(weights.lm_head, dt).T
+    f = rnd(h * weights.final_gain.astype(np.float64))
+    logits = (f @ to_f64(weights.lm_head, dt).T) * norm_scale(h, shape.rms_eps)
     return logits, block_kv

@@ -43,7 +43,7 @@ struct Layout {
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
-  size_t h, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, rowstat, ebuf, result, stage, rope, ws_total;
+  size_t h, ssq, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, rowstat, ebuf, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
   size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, s_eps, s_unif, s_sparam, stage_bytes;
   size_t kv_layer, kv_total;
@@ -125,6 +125,7 @@ Layout make_layout(const ee_model_config* c) {
   const size_t xcols = std::max(d, H * hd);
   o = 0;
   L.h = o; o += up(L.Rmax * d * 4);
+  L.ssq = o; o += up((size_t)L.Rmax * 8 * 4);
   L.xbuf = o; o += up(Tpad * xcols * esz);
   L.zbuf = o; o += up(Tpad * F * esz);
   L.q = o; o += up(L.Rmax * H * hd * esz);
@@ -230,6 +231,7 @@ void bind_work(ee_ctx* c) {
   unsigned char* ws = c->ws;
   ee::Work& w = c->w;
   w.h = reinterpret_cast<float*>(ws + L.h);
+  w.ssq = reinterpret_cast<float*>(ws + L.ssq);
   w.xbuf = reinterpret_cast<uint4*>(ws + L.xbuf);
   w.zbuf = reinterpret_cast<uint4*>(ws + L.zbuf);
   w.q = ws + L.q;

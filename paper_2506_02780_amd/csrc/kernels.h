@@ -61,6 +61,7 @@ struct Model {
 // sequence b); Rmax = max_seqs * (k_max + 1).
 struct Work {
   float* h;                 // [Rmax, d] residual stream
+  float* ssq;               // [Rmax, 8] sums of h^2 over 1024-column chunks (the norms' row scales)
   uint4* xbuf;              // packed activations, max(d, H*hd) columns
   uint4* zbuf;              // packed activations, F columns
   void* q;                  // [Rmax, H, hd] model dtype

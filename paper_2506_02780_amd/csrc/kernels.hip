@@ -339,6 +339,27 @@ __device__ __forceinline__ void store8(void* xout, int t, int col, int S, const 
   }
 }
 
+// Row scales of the split RMSNorm (see resid_kernel): chunk sums of h^2 per
+// 1024-column chunk of a row.
+constexpr int RES_THREADS = 128;               // 8 columns each
+constexpr int RES_COLS = RES_THREADS * 8;      // columns per workgroup
+constexpr int RES_MAX_PARTS = 8;               // chunks per row (d <= 8192)
+
+// RMS scale of row t: 1 / sqrt(sum of its chunk sums, in chunk order, / d + eps).
+// The row's chunk sums come with two 16-byte loads.
+__device__ __forceinline__ float row_scale(const float* __restrict__ ssq, int t, int d, float eps) {
+  static_assert(RES_MAX_PARTS == 8, "two 16-byte loads per row");
+  const float4 a = reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[0];
+  const float4 b = reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[1];
+  const float c[RES_MAX_PARTS] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  const int np = (d + RES_COLS - 1) / RES_COLS;
+  float s = c[0];
+#pragma unroll
+  for (int i = 1; i < RES_MAX_PARTS; ++i)
+    if (i < np) s += c[i];
+  return 1.0f / sqrtf(s / (float)d + eps);
+}
+
 // ------------------------------------------------------ gate/up + SwiGLU --
 //
 // For reductions of at most FK_MAX_S super-steps (d <= 4096 in bf16) the
@@ -363,11 +384,14 @@ __host__ __device__ inline int fk_groups(int R) { return R <= FK_GROUP + 1 ? 1 :
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
 
 struct FkArgs {
-  const uint4* w;   // packed [2F, d]: gate rows, then up rows
-  const uint4* x;   // packed activations of all R rows
-  void* z;          // packed [R, F] activations of the down projection
-  int S, n_pairs;   // super-steps of d; F / 16
-  int R, P, z_S;    // rows; workgroups per row group; super-steps of F
+  const uint4* w;     // packed [2F, d]: gate rows, then up rows
+  const uint4* x;     // packed activations of all R rows (h * gain of the FFN-side norm)
+  void* z;            // packed [R, F] activations of the down projection
+  int S, n_pairs;     // super-steps of d; F / 16
+  int R, P, z_S;      // rows; workgroups per row group; super-steps of F
+  const float* ssq;   // the norm's chunk sums of h^2 ([R][8]): row scales
+  int d;
+  float eps;
 };
 
 template <int DT, int MTV, int SPW>
@@ -415,6 +439,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   const int qq = threadIdx.x % (NR * 64);
   const bool qown = threadIdx.x < NR * 64;
   const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
+  const float rs = qown && rt < T ? row_scale(a.ssq, row0 + rt, a.d, a.eps) : 0.f;   // the norm's row scale
   f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
   uint4 wa[HA], wb[HB > 0 ? HB : 1];
 #pragma unroll
@@ -455,7 +480,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
       const int f = 16 * (g + (k >> 1) * a.P) + 4 * (rl >> 4);
       float zv[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) zv[r] = silu_mul(gate[r], v[r]);
+      for (int r = 0; r < 4; ++r) zv[r] = silu_mul(gate[r] * rs, v[r] * rs);
       const size_t fi = frag_index<DT>(row0 + rt, f, a.z_S);
       if (DT == DT_BF16) {
         *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.z) + fi) =
@@ -479,11 +504,14 @@ static void launch_gemm_swiglu(const FkArgs& a, int spw, dim3 grid, hipStream_t 
   }
 }
 
-// z = silu(x Wg^T) * (x Wu^T) for R rows, when d / KS <= FK_MAX_S.
+// z = silu(r x Wg^T) * (r x Wu^T) for R rows (r: each row's norm scale), when
+// d / KS <= FK_MAX_S.
 template <int DT>
-static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, int R, void* z, hipStream_t st) {
+static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, int R, void* z, const float* ssq,
+                              float eps, hipStream_t st) {
   FkArgs a;
   a.w = wgu; a.x = x; a.z = z;
+  a.ssq = ssq; a.d = d; a.eps = eps;
   a.S = d / Geo<DT>::KS;
   a.n_pairs = F / 16;
   a.R = R;
@@ -503,87 +531,64 @@ inline bool fused_swiglu(int d, int dt) { return d / ks_of(dt) <= FK_MAX_S; }
 
 // ------------------------------------------------------------ embed / norm --
 
-constexpr int NORM_THREADS = 512;
+// RMSNorm is split between this kernel and the consumers of the GEMM that
+// follows it: here the residual stream of row t is updated (h = E[tok] in
+// MODE 0, h += the GEMM slice partials in MODE 1), x = h * gain is stored,
+// rounded to the model dtype, as the next GEMM's packed activations, and the
+// sums of h^2 over the row's 1024-column chunks go to ssq[t][chunk]; the
+// consumer multiplies every output of row t by r = 1 / sqrt(sum h^2 / d + eps)
+// (row_scale), so RMSNorm(h) * gain * W = r * ((h * gain) W).  No workgroup
+// needs a whole row: a row's work spreads over d / 1024 workgroups.
 
-// Fixed-order sum of one float per thread over a NORM_THREADS block: an xor
-// butterfly inside each wave (every lane ends with the same bits), then the
-// wave sums in wave order.
-__device__ __forceinline__ float block_sum_norm(float v, float* sh) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-  __syncthreads();
-  float r = sh[0];
-#pragma unroll
-  for (int w = 1; w < NORM_THREADS / 64; ++w) r += sh[w];
-  return r;
-}
-
-// Row t of the residual stream: h = E[tok[t]] (MODE 0) or h += sum of the
-// GEMM slice partials (MODE 1); then x = RMSNorm(h) * gain, packed as the
-// next GEMM's activations.  Each thread owns up to two 8-column chunks
-// (d <= 8192, d % 8 == 0); every load is issued before the first use.
 template <int DT, int MODE>
-__global__ __launch_bounds__(NORM_THREADS) void norm_kernel(const void* __restrict__ embed,
+__global__ __launch_bounds__(RES_THREADS) void resid_kernel(const void* __restrict__ embed,
                                                             const int* __restrict__ tok, float* __restrict__ h,
                                                             const float* __restrict__ part, int SK, int T,
-                                                            const float* __restrict__ gain, float eps, int d,
-                                                            void* __restrict__ xout, int x_S) {
-  __shared__ float sh[NORM_THREADS / 64];
-  const int t = blockIdx.x;
-  float* hr = h + (size_t)t * d;
-  const int nch = d / 8;
-  constexpr int MAXCH = 2;
-  float v[MAXCH][8], gn[MAXCH][8];
-  const int row = MODE == 0 ? tok[t] : 0;
-#pragma unroll
-  for (int j = 0; j < MAXCH; ++j) {
-    const int ch = threadIdx.x + NORM_THREADS * j;
-    if (ch < nch) {
-      const int col = ch * 8;
-      const float4 g0 = *reinterpret_cast<const float4*>(gain + col);
-      const float4 g1 = *reinterpret_cast<const float4*>(gain + col + 4);
-      gn[j][0] = g0.x; gn[j][1] = g0.y; gn[j][2] = g0.z; gn[j][3] = g0.w;
-      gn[j][4] = g1.x; gn[j][5] = g1.y; gn[j][6] = g1.z; gn[j][7] = g1.w;
-      if (MODE == 0) {
-        const size_t e0 = (size_t)row * d + col;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[j][e] = load_elt<DT>(embed, e0 + e);
-      } else {
-        const float4 h0 = *reinterpret_cast<const float4*>(hr + col);
-        const float4 h1 = *reinterpret_cast<const float4*>(hr + col + 4);
-        const float4 p0 = sum_slices4(part, SK, T, d, t, col);
-        const float4 p1 = sum_slices4(part, SK, T, d, t, col + 4);
-        v[j][0] = h0.x + p0.x; v[j][1] = h0.y + p0.y; v[j][2] = h0.z + p0.z; v[j][3] = h0.w + p0.w;
-        v[j][4] = h1.x + p1.x; v[j][5] = h1.y + p1.y; v[j][6] = h1.z + p1.z; v[j][7] = h1.w + p1.w;
-      }
-    }
-  }
+                                                            const float* __restrict__ gain, int d,
+                                                            void* __restrict__ xout, int x_S,
+                                                            float* __restrict__ ssq) {
+  __shared__ float sh[RES_THREADS / 64];
+  const int t = blockIdx.y;
+  const int col = (blockIdx.x * RES_THREADS + threadIdx.x) * 8;
   float ss = 0.f;
+  if (col < d) {   // d % 8 == 0: a thread's 8 columns are all in range or all out
+    float* hr = h + (size_t)t * d + col;
+    float v[8];
+    if (MODE == 0) {
+      const size_t e0 = (size_t)tok[t] * d + col;
 #pragma unroll
-  for (int j = 0; j < MAXCH; ++j) {
-    const int ch = threadIdx.x + NORM_THREADS * j;
-    if (ch < nch) {
-      const int col = ch * 8;
-      *reinterpret_cast<float4*>(hr + col) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
-      *reinterpret_cast<float4*>(hr + col + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ss = fmaf(v[j][e], v[j][e], ss);
+      for (int e = 0; e < 8; ++e) v[e] = load_elt<DT>(embed, e0 + e);
+    } else {
+      const float4 h0 = *reinterpret_cast<const float4*>(hr), h1 = *reinterpret_cast<const float4*>(hr + 4);
+      const float4 p0 = sum_slices4(part, SK, T, d, t, col), p1 = sum_slices4(part, SK, T, d, t, col + 4);
+      v[0] = h0.x + p0.x; v[1] = h0.y + p0.y; v[2] = h0.z + p0.z; v[3] = h0.w + p0.w;
+      v[4] = h1.x + p1.x; v[5] = h1.y + p1.y; v[6] = h1.z + p1.z; v[7] = h1.w + p1.w;
     }
+    const float4 g0 = *reinterpret_cast<const float4*>(gain + col), g1 = *reinterpret_cast<const float4*>(gain + col + 4);
+    const float gn[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    *reinterpret_cast<float4*>(hr) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(hr + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ss = fmaf(v[e], v[e], ss);
+      o[e] = v[e] * gn[e];
+    }
+    store8<DT>(xout, t, col, x_S, o);
   }
-  ss = block_sum_norm(ss, sh);
-  const float r = 1.0f / sqrtf(ss / (float)d + eps);
+  // fixed-order chunk sum: xor butterfly inside each wave, then the waves in order
 #pragma unroll
-  for (int j = 0; j < MAXCH; ++j) {
-    const int ch = threadIdx.x + NORM_THREADS * j;
-    if (ch < nch) {
-      float o[8];
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float r = sh[0];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = v[j][e] * r * gn[j][e];
-      store8<DT>(xout, t, ch * 8, x_S, o);
-    }
+    for (int w = 1; w < RES_THREADS / 64; ++w) r += sh[w];
+    ssq[t * RES_MAX_PARTS + blockIdx.x] = r;
   }
 }
+
 
 // q/k/v of row t from the QKV partials: rotary on q and k (pairs (i, i+hd/2)
 // at the row's position), q to the block buffer, k and v into the row's KV
@@ -595,7 +600,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
                                                          const int* __restrict__ pos,
                                                          const float2* __restrict__ rope,
                                                          const int* __restrict__ rowslot,
-                                                         void* __restrict__ q, void* __restrict__ kv_layer) {
+                                                         void* __restrict__ q, void* __restrict__ kv_layer,
+                                                         const float* __restrict__ ssq, int d, float eps) {
   const int t = blockIdx.y;
   const int half = hd >> 1;
   const int pairs = (H + 2 * Hkv) * half;
@@ -614,6 +620,9 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
 #pragma unroll
   for (int k = 1; k < MAX_SLICES; ++k)
     if (k < SK) { x1 += p1[k]; x2 += p2[k]; }
+  const float rs = row_scale(ssq, t, d, eps);   // the input norm's row scale
+  x1 *= rs;
+  x2 *= rs;
   const int slot = rowslot[t];
   const int page = slot >> 6, sp = slot & 63;
   if (head < H + Hkv) {
@@ -640,7 +649,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
 // up), packed as the down projection's activations.  8 features per thread.
 template <int DT>
 __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ part, int SK, int T, int F,
-                                                     void* __restrict__ zout, int z_S) {
+                                                     void* __restrict__ zout, int z_S,
+                                                     const float* __restrict__ ssq, int d, float eps) {
   const int t = blockIdx.y;
   const int ch = blockIdx.x * 256 + threadIdx.x;
   if (ch * 8 >= F) return;
@@ -650,8 +660,9 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ p
   const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
   const float u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
   float z[8];
+  const float rs = row_scale(ssq, t, d, eps);   // the input norm's row scale
 #pragma unroll
-  for (int e = 0; e < 8; ++e) z[e] = silu_mul(g[e], u[e]);
+  for (int e = 0; e < 8; ++e) z[e] = silu_mul(g[e] * rs, u[e] * rs);
   store8<DT>(zout, t, f, z_S, z);
 }
 
@@ -702,18 +713,23 @@ __device__ __forceinline__ void wave_top8(unsigned long long (&k)[8], unsigned l
   }
 }
 
-// Logits of row t from the LM-head partials, plus, per 2048-column chunk,
+// Logits of row t from the LM-head partials (times the final norm's row
+// scale), plus, per 2048-column chunk,
 // either the largest key (TOPK false: amax[t][chunk]) or the 8 largest keys
 // in descending order (TOPK true: amax[t][chunk][8]).
 template <bool TOPK>
 __global__ __launch_bounds__(256) void logits_kernel(const float* __restrict__ part, int SK, int T, int V,
                                                      float* __restrict__ logits,
-                                                     unsigned long long* __restrict__ amax, int nchunk) {
+                                                     unsigned long long* __restrict__ amax, int nchunk,
+                                                     const float* __restrict__ ssq, int d, float eps) {
   const int t = blockIdx.y;
   const int col = (blockIdx.x * 256 + threadIdx.x) * 8;
   unsigned long long key[8] = {0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull, 0ull};
   if (col < V) {   // V is a multiple of 16: a thread's 8 columns are all in range or all out
-    const float4 a = sum_slices4(part, SK, T, V, t, col), b = sum_slices4(part, SK, T, V, t, col + 4);
+    const float rs = row_scale(ssq, t, d, eps);   // the final norm's row scale
+    float4 a = sum_slices4(part, SK, T, V, t, col), b = sum_slices4(part, SK, T, V, t, col + 4);
+    a.x *= rs; a.y *= rs; a.z *= rs; a.w *= rs;
+    b.x *= rs; b.y *= rs; b.z *= rs; b.w *= rs;
     float* lr = logits + (size_t)t * V + col;
     *reinterpret_cast<float4*>(lr) = a;
     *reinterpret_cast<float4*>(lr + 4) = b;
@@ -1915,8 +1931,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   auto last = [] { return hipGetLastError(); };
 
   if ((e = timed(prof, PC_NORM, st, [&] {
-         hipLaunchKernelGGL((norm_kernel<DT, 0>), dim3(R), dim3(NORM_THREADS), 0, st, m.embed, w.tok, w.h,
-                            w.part, 1, R, m.layers[0].attn_gain, m.eps, d, (void*)w.xbuf, Sd);
+         hipLaunchKernelGGL((resid_kernel<DT, 0>), dim3((d + RES_COLS - 1) / RES_COLS, R), dim3(RES_THREADS), 0, st,
+                            m.embed, w.tok, w.h, w.part, 1, R, m.layers[0].attn_gain, d, (void*)w.xbuf, Sd, w.ssq);
          return last();
        })) != hipSuccess)
     return e;
@@ -1934,7 +1950,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
            hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, R), dim3(256), 0, st, w.part,
-                              sk_d, R, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.slot, w.q, kvl);
+                              sk_d, R, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.slot, w.q, kvl, w.ssq, d, m.eps);
            return last();
          })) != hipSuccess)
       return e;
@@ -1979,8 +1995,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(R), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
-                              sk_q, R, lp.ffn_gain, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((resid_kernel<DT, 1>), dim3((d + RES_COLS - 1) / RES_COLS, R), dim3(RES_THREADS), 0,
+                              st, nullptr, nullptr, w.h, w.part, sk_q, R, lp.ffn_gain, d, (void*)w.xbuf, Sd, w.ssq);
            return last();
          })) != hipSuccess)
       return e;
@@ -1988,7 +2004,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     // split-K partials and a SwiGLU launch
     if (fused_swiglu(d, DT)) {
       if ((e = timed(prof, PC_GATEUP, st, [&] {
-             return gemm_swiglu<DT>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st);
+             return gemm_swiglu<DT>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st);
            })) != hipSuccess)
         return e;
     } else {
@@ -1997,7 +2013,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
         return e;
       if ((e = timed(prof, PC_FINISH, st, [&] {
              hipLaunchKernelGGL((swiglu_kernel<DT>), dim3((m.F / 8 + 255) / 256, R), dim3(256), 0, st, w.part, sk_d,
-                                R, m.F, (void*)w.zbuf, Sf);
+                                R, m.F, (void*)w.zbuf, Sf, w.ssq, d, m.eps);
              return last();
            })) != hipSuccess)
         return e;
@@ -2007,8 +2023,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     const float* gn = (l + 1 < m.L) ? m.layers[l + 1].attn_gain : m.final_gain;
     if ((e = timed(prof, PC_NORM, st, [&] {
-           hipLaunchKernelGGL((norm_kernel<DT, 1>), dim3(R), dim3(NORM_THREADS), 0, st, nullptr, nullptr, w.h, w.part,
-                              sk_f, R, gn, m.eps, d, (void*)w.xbuf, Sd);
+           hipLaunchKernelGGL((resid_kernel<DT, 1>), dim3((d + RES_COLS - 1) / RES_COLS, R), dim3(RES_THREADS), 0,
+                              st, nullptr, nullptr, w.h, w.part, sk_f, R, gn, d, (void*)w.xbuf, Sd, w.ssq);
            return last();
          })) != hipSuccess)
       return e;
@@ -2021,10 +2037,10 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   if ((e = timed(prof, PC_FINISH, st, [&] {
          if (topk)
            hipLaunchKernelGGL(logits_kernel<true>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
-                              w.logits, w.amax, nchunk);
+                              w.logits, w.amax, nchunk, w.ssq, d, m.eps);
          else
            hipLaunchKernelGGL(logits_kernel<false>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
-                              w.logits, w.amax, nchunk);
+                              w.logits, w.amax, nchunk, w.ssq, d, m.eps);
          return last();
        })) != hipSuccess)
     return e;
@@ -2072,8 +2088,8 @@ hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hi
                             : gemm<DT_F32>(lp.wo, w.xbuf, d, qdim, R, w.part, st); break;
       case PC_GATEUP:
         if (fused_swiglu(d, m.dt))
-          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st)
-                 : gemm_swiglu<DT_F32>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, st);
+          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st)
+                 : gemm_swiglu<DT_F32>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st);
         else
           e = bf ? gemm<DT_BF16>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st)
                  : gemm<DT_F32>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st);

@@ -95,7 +95,10 @@ def test_topk_session_matches_oracle(ee, cfg, k, dynamic):
     assert eng.prefill(0, prompt) == ref.prefill(prompt)
     g = np.random.default_rng(k + 10 * dynamic)
     seen, pinned, accepted_beyond_greedy = [], 0, 0
-    for step in range(8):
+    # bf16 logits are ~0.04 apart from the oracle's, so few rows have a unique
+    # dynamic threshold (k H must lie 3 k err from an integer): more steps
+    steps = 8 if cfg == "f32" else 24
+    for step in range(steps):
         K = int(g.integers(0, 13)) if step else 0
         draft = _ranked_draft(ref, K, g)
         res = eng.verify_topk([0], [draft], k, dynamic)[0]
@@ -108,7 +111,7 @@ def test_topk_session_matches_oracle(ee, cfg, k, dynamic):
     eng.close()
     print(f"pinned {pinned} steps, {len(seen)} thresholds compared, values {sorted(set(seen))}")
     if cfg == "f32":
-        assert pinned == 8
+        assert pinned == steps
         assert len(seen) >= 30
         assert accepted_beyond_greedy >= 3
         if dynamic:

@@ -130,3 +130,16 @@ def test_gqa_groups_are_contiguous():
     mask = np.ones((5, 9), dtype=bool)
     mha = attention(q, np.repeat(k, 2, axis=1), np.repeat(v, 2, axis=1), mask, 0.5)
     np.testing.assert_allclose(attention(q, k, v, mask, 0.5), mha, rtol=1e-13)
+
+
+def test_norm_scale_times_gained_input_is_rmsnorm():
+    """The split form used before a projection: r * (h * g) with r the row's
+    RMS scale equals RMSNorm(h) * g, with r from torch's rms_norm of a ones
+    gain as an independent reference."""
+    from oracle.model import norm_scale
+    g = np.random.default_rng(4)
+    h = g.standard_normal((5, 192)) * 3.0
+    gain = 1.0 + 0.1 * g.standard_normal(192)
+    np.testing.assert_allclose(norm_scale(h, 1e-5) * (h * gain), rmsnorm(h, gain, 1e-5), rtol=1e-13)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(h), (192,), torch.ones(192, dtype=torch.float64), 1e-5)
+    np.testing.assert_allclose(norm_scale(h, 1e-5) * h, ref.numpy(), rtol=1e-12)
