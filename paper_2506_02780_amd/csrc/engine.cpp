@@ -149,7 +149,7 @@ Layout make_layout(const ee_model_config* c) {
   L.rowstat = o; o += up((size_t)L.Rmax * 2 * 8);
   L.ebuf = o; o += up((size_t)L.Rmax * V * 8);
   L.result = o; o += up((size_t)c->max_seqs * (2 + c->k_max) * 4);
-  // staging block: one host->device copy per call
+  // staging block: read from its pinned host mirror by the block's first kernel
   size_t so = 0;
   L.s_tok = so; so += L.Rmax * 4;
   L.s_pos = so; so += L.Rmax * 4;
@@ -199,6 +199,8 @@ struct ee_ctx {
   std::vector<int> free_pages;
   unsigned char* h_stage = nullptr;   // pinned mirror of the staging block
   int* h_result = nullptr;            // pinned
+  uint32_t* d_stage_src = nullptr;    // device-visible addresses of h_stage and h_result
+  int* d_result_dst = nullptr;
   int last_T = 0;
   std::string err = "no error";
   // profiling
@@ -289,13 +291,45 @@ int check_seq(ee_ctx* c, int seq) {
   return EE_OK;
 }
 
-// The kernels of one block, in launch order.
+// The staging words a block of this shape reads: the rows' tokens, positions,
+// parents and slots, the trees' paths, the sequences' page tables and step
+// state, and the draws and parameters of stochastic verification.
+ee::StageCopy stage_ranges(const ee_ctx* c, const ee::Step& step) {
+  const Layout& L = c->lay;
+  ee::StageCopy sc{};
+  sc.src = c->d_stage_src;
+  sc.dst = reinterpret_cast<uint32_t*>(c->ws + L.stage);
+  const size_t R = (size_t)step.B * step.T;
+  auto add = [&](size_t off, size_t words) {
+    sc.off[sc.n] = (int)(off / 4);
+    sc.len[sc.n] = (int)words;
+    sc.total += (int)words;
+    ++sc.n;
+  };
+  add(L.s_tok, R);
+  add(L.s_pos, R);
+  add(L.s_prow, R);
+  add(L.s_slot, R);
+  if (step.mode == 2) add(L.s_path, R * 16);
+  add(L.s_ptable, (size_t)step.B * L.ptable_len);
+  add(L.s_info, (size_t)step.B * 4);
+  if (step.mode == 4) {
+    add(L.s_eps, R);
+    add(L.s_unif, R);
+    add(L.s_sparam, 4);
+  }
+  return sc;
+}
+
+// The kernels of one block, in launch order: staging in, forward, acceptance
+// (+ tree compaction), results out.
 hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
   hipError_t e;
+  if ((e = ee::run_stage_in(stage_ranges(c, step), c->st)) != hipSuccess) return e;
   if ((e = ee::run_forward(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
   if ((e = ee::run_accept(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
   if (step.mode == 2 && (e = ee::run_compact(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
-  return hipSuccess;
+  return ee::run_result_out(c->w, step.B, c->d_result_dst, c->st);
 }
 
 // Captured graph of a (T, mode) block shape, built on first use (profiling
@@ -329,10 +363,11 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
 }
 
 // Stage the per-sequence state (page tables, committed lengths, the KV slot
-// of every row), run the forward + acceptance (+ tree compaction) of B
-// sequences of T rows whose tokens, positions and parents the caller staged,
-// and fetch the results (record b at h_result + b * (2 + k_max)).  Mode 3 uses
-// the top-k size and dynamic flag given for every sequence.
+// of every row) in the pinned mirror, run the block of B sequences of T rows
+// whose tokens, positions and parents the caller staged (its kernels read the
+// mirror and write the results to h_result, record b at h_result + b *
+// (2 + k_max)) and wait for it.  Mode 3 uses the top-k size and dynamic flag
+// given for every sequence.
 int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0, int dynamic = 0) {
   const Layout& L = c->lay;
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
@@ -352,7 +387,6 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
   }
   HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
   HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
-  HIP_TRY(c, hipMemcpyAsync(c->ws + L.stage, c->h_stage, L.stage_bytes, hipMemcpyHostToDevice, c->st));
   const ee::Step step{T, B, mode};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
@@ -364,8 +398,6 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
     c->prof.used = 0;
     HIP_TRY(c, launch_block(c, step, prof));
   }
-  HIP_TRY(c, hipMemcpyAsync(c->h_result, c->w.result, (size_t)B * c->w.rec * sizeof(int),
-                            hipMemcpyDeviceToHost, c->st));
   HIP_TRY(c, hipStreamSynchronize(c->st));
   for (int i = 0; prof && i < c->prof.used; ++i) {
     float ms = 0.f;
@@ -576,6 +608,11 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
     return cleanup(EE_EHIP);
   }
   memset(c->h_stage, 0, L.stage_bytes);
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->d_stage_src), c->h_stage, 0)) != hipSuccess ||
+      (e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->d_result_dst), c->h_result, 0)) != hipSuccess) {
+    hip_fail(c, e, "hipHostGetDevicePointer");
+    return cleanup(EE_EHIP);
+  }
 
   // pack weights
   auto run = [&](hipError_t err, const char* where) {

@@ -119,6 +119,21 @@ enum ProfClass {
   PC_ACCEPT, PC_COMPACT, PC_FINISH, PC_N
 };
 
+// Word ranges copied from the pinned host mirror of the staging block into the
+// device staging block by the first kernel of a block (the same word offsets
+// on both sides).
+struct StageCopy {
+  const uint32_t* src;      // host mirror (device-visible address)
+  uint32_t* dst;            // device staging block
+  int n;                    // ranges in use
+  int off[10], len[10];     // word offset and word count of each range
+  int total;                // sum of the word counts
+};
+hipError_t run_stage_in(const StageCopy& sc, hipStream_t st);
+// The result records of B sequences (B * rec ints) copied from the device to
+// pinned host memory (device-visible address) by the last kernel of a block.
+hipError_t run_result_out(const Work& w, int B, int* host_result, hipStream_t st);
+
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);

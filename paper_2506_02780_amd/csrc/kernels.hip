@@ -2057,6 +2057,39 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   });
 }
 
+// ------------------------------------------------------------ host staging --
+//
+// The per-call inputs are read straight from pinned host memory and the
+// result records written straight back to it by kernels of the block itself,
+// so a block waits on no copy-engine transfer before its first kernel or
+// after its last.
+
+__global__ __launch_bounds__(256) void stage_in_kernel(StageCopy sc) {
+  int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= sc.total) return;
+  int r = 0;
+  while (r + 1 < sc.n && i >= sc.len[r]) i -= sc.len[r++];
+  sc.dst[sc.off[r] + i] = sc.src[sc.off[r] + i];
+}
+
+__global__ __launch_bounds__(256) void result_out_kernel(const int* __restrict__ src, int* dst, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+  __threadfence_system();
+}
+
+hipError_t run_stage_in(const StageCopy& sc, hipStream_t st) {
+  if (sc.total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(stage_in_kernel, dim3((sc.total + 255) / 256), dim3(256), 0, st, sc);
+  return hipGetLastError();
+}
+
+hipError_t run_result_out(const Work& w, int B, int* host_result, hipStream_t st) {
+  const int n = B * w.rec;
+  hipLaunchKernelGGL(result_out_kernel, dim3((n + 255) / 256), dim3(256), 0, st, w.result, host_result, n);
+  return hipGetLastError();
+}
+
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
   if (m.dt == DT_BF16 && m.hd == 128) return forward_t<DT_BF16, 128>(m, w, s, prof, st);
   if (m.dt == DT_BF16 && m.hd == 64) return forward_t<DT_BF16, 64>(m, w, s, prof, st);
