@@ -90,8 +90,10 @@ size_t ee_workspace_bytes(const ee_model_config* cfg);
 
 /* Build a context.  Packs every weight into `packed` (the library's
  * MFMA-fragment layout) and zeroes `kv_pool`, on `hip_stream` (a hipStream_t;
- * NULL = the default stream), then synchronizes that stream.  All later GPU
- * work of the context runs on the same stream. */
+ * NULL = the default stream), then synchronizes that stream.  Every later
+ * call runs its GPU work on a stream of the context's own, ordered after the
+ * work enqueued on `hip_stream` when the call starts, and returns once that
+ * work is done. */
 int32_t ee_create(const ee_model_config* cfg, const ee_weights* w, void* packed,
                   void* kv_pool, void* workspace, void* hip_stream, ee_ctx** out);
 int32_t ee_destroy(ee_ctx* ctx);

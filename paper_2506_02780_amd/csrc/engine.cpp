@@ -385,8 +385,14 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
       slot[b * T + t] = s.pages[p / PAGE] * PAGE + p % PAGE;
     }
   }
-  HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
-  HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
+  // order the block after the caller's stream; an idle stream (the usual case)
+  // needs no event, whose record and wait cost ~15 us of host time per call
+  const hipError_t q = hipStreamQuery(c->user_st);
+  if (q != hipSuccess) {
+    if (q != hipErrorNotReady) return hip_fail(c, q, "hipStreamQuery");
+    HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
+    HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
+  }
   const ee::Step step{T, B, mode};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
