@@ -287,6 +287,20 @@ int32_t ee_get_logits(ee_ctx* ctx, float* host_out, int32_t rows);
  * dtype (fp32 or bf16 bits).  Either output may be NULL.  Test aid. */
 int32_t ee_read_kv(ee_ctx* ctx, int32_t seq, int32_t layer, void* host_k, void* host_v);
 
+/* Install a committed cache in the empty sequence `seq`: keys and values of
+ * positions [0, n) of every layer from host memory, [n_layers][n][n_kv_heads]
+ * [head_dim] each in the model dtype (fp32 or bf16 bits; the caller keeps
+ * ownership), and `pending` as the token the next block starts with.  The
+ * sequence is then as if a prefill of n tokens had produced this cache and
+ * greedy token (the Eq. 3 prefix of later blocks).  Errors (EE_EINVAL for
+ * NULL arrays, n < 1 or a pending token outside [0, vocab); EE_ESTATE if the
+ * sequence holds tokens; EE_ECAPACITY if n + 1 > max_ctx or the KV pool is
+ * short) leave the sequence empty.  Synchronous.  The counterpart of
+ * ee_read_kv: a test aid, and a way to resume from a cache computed
+ * elsewhere. */
+int32_t ee_load_kv(ee_ctx* ctx, int32_t seq, int32_t n, int32_t pending, const void* host_k,
+                   const void* host_v);
+
 /* Launch mode of later prefill/verify blocks.  on != 0 (the default): the
  * kernels of each block shape (row count, linear/tree/prefill) are captured
  * once into a HIP graph and replayed; on == 0: every kernel is launched

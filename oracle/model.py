@@ -120,7 +120,7 @@ def tree_structure(parent):
     return depth, vis
 
 
-def forward_block(shape, weights, cache, tokens, depth, vis):
+def forward_block(shape, weights, cache, tokens, depth, vis, rounding_noise=None):
     """One forward of the target model over a block.
 
     shape   : model shape (n_layers, d_model, n_heads, n_kv_heads, head_dim,
@@ -130,10 +130,24 @@ def forward_block(shape, weights, cache, tokens, depth, vis):
               in the model dtype, logical [out, in] layout
     cache   : list per layer of (K, V), float64 [n, Hkv, hd] (already rounded)
     tokens  : [T] token ids; depth: [T]; vis: [T, T] bool
+    rounding_noise : None (the definition above) or (generator, rel), a
+              sensitivity probe for tests: every value rounded to bf16 is first
+              multiplied by 1 + rel * N(0, 1), an error of the size a float32
+              evaluation of the same expression carries.  The spread this
+              causes in the logits is the part of a bf16 pipeline's result that
+              its rounding points leave open (an operand within float32 error of
+              a rounding boundary may round either way).
     Returns (logits [T, vocab] float64, block_kv: list per layer of (k, v) [T, Hkv, hd]).
     """
     dt = shape.dtype
     rnd = _rounder(dt)
+    if rounding_noise is not None and dt == "bf16":
+        gen, rel = rounding_noise
+        exact = rnd
+
+        def rnd(a):
+            a = np.asarray(a, dtype=np.float64)
+            return exact(a * (1.0 + rel * gen.standard_normal(a.shape)))
     H, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     tokens = np.asarray(tokens, dtype=np.int64)
     t = len(tokens)

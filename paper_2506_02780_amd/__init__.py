@@ -70,6 +70,7 @@ ee_seq_state = _sig("ee_seq_state", _i32, [_vp, _i32, _pi32, _pi32])
 ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32, _i32, _i32, _pi32, _pi32])
 ee_get_logits = _sig("ee_get_logits", _i32, [_vp, ctypes.POINTER(ctypes.c_float), _i32])
 ee_read_kv = _sig("ee_read_kv", _i32, [_vp, _i32, _i32, _vp, _vp])
+ee_load_kv = _sig("ee_load_kv", _i32, [_vp, _i32, _i32, _i32, _vp, _vp])
 ee_last_error = _sig("ee_last_error", ctypes.c_char_p, [_vp])
 ee_profile = _sig("ee_profile", _i32, [_vp, ctypes.c_uint32])
 ee_use_graphs = _sig("ee_use_graphs", _i32, [_vp, _i32])
@@ -321,6 +322,18 @@ class Engine:
         v = np.empty_like(k)
         _check(ee_read_kv(self.ctx, seq, layer, k.ctypes.data, v.ctypes.data), self.ctx)
         return k, v
+
+    def load_kv(self, seq: int, k, v, pending: int):
+        """Install a committed cache in the empty sequence `seq`: k and v are
+        [n_layers, n, n_kv_heads, head_dim] in the model dtype (bf16 bit
+        patterns as uint16, or float32); `pending` starts the next block."""
+        s = self.shape
+        dt = np.uint16 if s.dtype == "bf16" else np.float32
+        k = np.ascontiguousarray(k, dtype=dt)
+        v = np.ascontiguousarray(v, dtype=dt)
+        if k.shape != v.shape or k.ndim != 4 or k.shape[0] != s.n_layers or k.shape[2:] != (s.n_kv_heads, s.head_dim):
+            raise EEError(EE_EINVAL, "k and v must be [n_layers, n, n_kv_heads, head_dim]")
+        _check(ee_load_kv(self.ctx, seq, k.shape[1], int(pending), k.ctypes.data, v.ctypes.data), self.ctx)
 
     def use_graphs(self, on: bool):
         """Replay captured HIP graphs per block shape (default) or launch eagerly."""

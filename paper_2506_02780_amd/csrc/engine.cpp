@@ -905,6 +905,51 @@ int32_t ee_read_kv(ee_ctx* c, int32_t seq, int32_t layer, void* host_k, void* ho
   return EE_OK;
 }
 
+int32_t ee_load_kv(ee_ctx* c, int32_t seq, int32_t n, int32_t pending, const void* host_k, const void* host_v) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!host_k || !host_v) return fail(c, EE_EINVAL, "host_k and host_v must be non-NULL");
+  if (n < 1) return fail(c, EE_EINVAL, "n must be >= 1");
+  if (pending < 0 || pending >= c->cfg.vocab) return fail(c, EE_EINVAL, "pending token outside [0, vocab)");
+  Seq& s = c->seqs[seq];
+  if (s.live) return fail(c, EE_ESTATE, "sequence already holds tokens (roll it back to 0 first)");
+  if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "cache longer than max_ctx - 1");
+  int added;
+  if (!reserve_pages(c, s, n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  const size_t esz = c->cfg.dtype == EE_BF16 ? 2 : 4;
+  const int Hkv = c->cfg.n_kv_heads, hd = c->cfg.head_dim;
+  const size_t blk = (size_t)PAGE * hd * esz;            // one (page, kv, head) block
+  const size_t layer_in = (size_t)n * Hkv * hd * esz;     // one layer of host_k / host_v
+  std::vector<unsigned char> page(2 * Hkv * blk);
+  for (int layer = 0; layer < c->cfg.n_layers; ++layer)
+    for (size_t pi = 0; pi < s.pages.size(); ++pi) {
+      // K rows [slot][dim] and V^T [dim][slot] of this page; slots past n stay zero
+      std::fill(page.begin(), page.end(), 0);
+      for (int sp = 0; sp < PAGE && (int)(pi * PAGE) + sp < n; ++sp) {
+        const size_t slot = pi * PAGE + sp;
+        for (int g = 0; g < Hkv; ++g)
+          for (int dim = 0; dim < hd; ++dim) {
+            const size_t src = layer * layer_in + ((slot * Hkv + g) * hd + dim) * esz;
+            memcpy(page.data() + (0 * Hkv + g) * blk + ((size_t)sp * hd + dim) * esz,
+                   reinterpret_cast<const unsigned char*>(host_k) + src, esz);
+            memcpy(page.data() + (1 * Hkv + g) * blk + ((size_t)dim * PAGE + sp) * esz,
+                   reinterpret_cast<const unsigned char*>(host_v) + src, esz);
+          }
+      }
+      unsigned char* dst = c->pool + layer * c->lay.kv_layer + (size_t)s.pages[pi] * 2 * Hkv * blk;
+      hipError_t e = hipMemcpyAsync(dst, page.data(), page.size(), hipMemcpyHostToDevice, c->st);
+      if (e == hipSuccess) e = hipStreamSynchronize(c->st);   // the page buffer is refilled next
+      if (e != hipSuccess) {
+        unreserve(c, s, added);
+        return hip_fail(c, e, "hipMemcpy");
+      }
+    }
+  s.len = n;
+  s.live = true;
+  s.pending = pending;
+  return EE_OK;
+}
+
 int32_t ee_use_graphs(ee_ctx* c, int32_t on) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
   c->graphs_on = on != 0;

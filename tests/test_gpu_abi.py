@@ -76,3 +76,37 @@ def test_time_gemm_measurement_aid(ee, eng):
             eng.time_gemm(*bad)
         assert e.value.code == ee.EE_EINVAL
     assert eng.seq_state(0) == n0
+
+
+def test_load_kv_round_trip_errors_and_parity(ee, eng):
+    """ee_load_kv installs a cache that ee_read_kv returns unchanged; a block
+    over it matches the oracle over the same cache (fp32, 1e-4); errors leave
+    the sequence empty."""
+    from oracle import OracleSession
+    from workloads import random_kv_context
+    shape = get_shape("tiny")
+    n = 150   # three pages, the last one partly filled
+    kv = random_kv_context(shape.n_layers, n, shape.n_kv_heads, shape.head_dim, seed=8, dtype="f32")
+    k = np.stack([a for a, _ in kv])
+    v = np.stack([b for _, b in kv])
+    _expect(ee, ee.EE_EINVAL, eng.load_kv, 1, k, v, shape.vocab)       # pending outside [0, vocab)
+    _expect(ee, ee.EE_ECAPACITY, eng.load_kv, 1,
+            np.zeros((shape.n_layers, 200, shape.n_kv_heads, shape.head_dim), np.float32),
+            np.zeros((shape.n_layers, 200, shape.n_kv_heads, shape.head_dim), np.float32), 3)   # n + 1 > max_ctx
+    assert eng.seq_state(1) == (0, -1)
+    eng.load_kv(1, k, v, 17)
+    assert eng.seq_state(1) == (n, 17)
+    _expect(ee, ee.EE_ESTATE, eng.load_kv, 1, k, v, 17)                 # not empty
+    for l in range(shape.n_layers):
+        rk, rv = eng.read_kv(1, l)
+        np.testing.assert_array_equal(rk, k[l])
+        np.testing.assert_array_equal(rv, v[l])
+    w = gen_weights(shape, seed=9, std=0.1)   # the engine's weights
+    ref = OracleSession(shape, w)
+    ref.set_cache([(a.astype(np.float64), b.astype(np.float64)) for a, b in kv], 17)
+    d = zipf_tokens(shape.vocab, 8, seed=6)
+    ra, rn, _ = ref.verify(d)
+    a, nxt, _ = eng.verify(1, d)
+    np.testing.assert_allclose(eng.logits(), ref.last_logits, rtol=0, atol=1e-4)
+    assert (a, nxt) == (ra, rn)
+    eng.rollback(1, 0, -1)

@@ -1,0 +1,136 @@
+"""Full-size checks in the configuration the benchmark times: the 7B-class
+bf16 decoder (32 layers, d_model 4096, 32 query / 8 KV heads, FFN 11008,
+vocab 32256), verify blocks of T = 33 rows (K = 32) over a 2048-position
+committed context, replayed from captured graphs.
+
+* Parity with the oracle: the committed context is a seeded random bf16 cache
+  installed on both sides (``ee_load_kv`` / ``OracleSession.set_cache``), so
+  the oracle needs no 2048-token prefill.  Two verify blocks are compared:
+  every logit of all 33 rows, and the acceptance exact wherever the oracle's
+  top-2 margins decide it.  The bound is max-abs 2e-2 or, where larger, twice
+  the oracle's own spread: the largest logit change of the oracle when each
+  value it rounds to bf16 carries a float32-sized relative error (2^-23
+  N(0, 1)).  At this depth that spread is ~0.12: an operand within float32
+  error of a bf16 rounding boundary rounds either way, and 32 layers of such
+  flips move the logits of this random model by ~9% of their spread, for any
+  evaluation that is not the exact one.
+* Properties that need no oracle, after a real 2048-token prefill: the
+  speculative stream equals the GPU's own token-by-token greedy loop bit for
+  bit (the lossless property of greedy verification, Eq. 7), and the rows of a
+  33-row block carry bitwise the logits of the single-row blocks at the same
+  positions.
+"""
+
+import numpy as np
+import pytest
+
+from helpers import assert_step_matches
+from oracle import OracleSession, greedy_rows
+from oracle.numerics import to_f64
+from workloads import gen_weights, get_shape, planted_draft, random_kv_context, zipf_tokens
+
+pytestmark = pytest.mark.gpu
+
+CTX, K = 2048, 32
+TOL = 2e-2          # bf16 logits, max-abs against the fp64 oracle
+NOISE = 2.0 ** -23  # relative error of the oracle's sensitivity probe
+
+
+@pytest.fixture(scope="module")
+def ee():
+    import paper_2506_02780_amd as mod
+    return mod
+
+
+@pytest.fixture(scope="module")
+def model(ee):
+    shape = get_shape("7b")
+    print(f"[fullsize] drawing {shape.name} weights", flush=True)
+    w = gen_weights(shape, seed=1234)
+    eng = ee.Engine(shape, w, max_ctx=CTX + 128, k_max=K)
+    yield shape, w, eng
+    eng.close()
+
+
+def _oracle_block(shape, w, cache, pending, draft):
+    """(exact oracle session after the block, its accept length and next
+    token, bound): the bound is 2e-2 or twice the largest logit change under
+    the rounding-noise probe."""
+    ref = OracleSession(shape, w)
+    ref.set_cache(cache, pending)
+    ra, rn, _ = ref.verify(draft)
+    probe = OracleSession(shape, w, rounding_noise=(np.random.default_rng(7), NOISE))
+    probe.set_cache(cache, pending)
+    probe.verify(draft)
+    spread = float(np.abs(probe.last_logits - ref.last_logits).max())
+    print(f"[fullsize] oracle spread under rounding noise {spread:.4f}", flush=True)
+    return ref, ra, rn, max(TOL, 2.0 * spread)
+
+
+def _check(eng, a, nxt, ref, ra, rn, tol):
+    err = float(np.abs(eng.logits() - ref.last_logits).max())
+    print(f"[fullsize] max |GPU - oracle| {err:.4f}, bound {tol:.4f}", flush=True)
+    assert_step_matches(eng.logits(), a, nxt, ref.last_logits, ra, rn, K, tol)
+
+
+def test_7b_k32_blocks_over_2048_positions_match_oracle(model):
+    shape, w, eng = model
+    kv = random_kv_context(shape.n_layers, CTX, shape.n_kv_heads, shape.head_dim, seed=5, dtype="bf16")
+    pending = int(zipf_tokens(shape.vocab, 1, seed=11)[0])
+    cache = [(to_f64(k, "bf16"), to_f64(v, "bf16")) for k, v in kv]
+    eng.rollback(0, 0, -1)
+    eng.load_kv(0, np.stack([k for k, _ in kv]), np.stack([v for _, v in kv]), pending)
+    del kv
+    assert eng.seq_state(0) == (CTX, pending)
+
+    # block 1: a Zipf draft
+    d1 = zipf_tokens(shape.vocab, K, seed=12)
+    print("[fullsize] oracle block 1", flush=True)
+    ref, ra, rn, tol = _oracle_block(shape, w, cache, pending, d1)
+    g1 = greedy_rows(ref.last_logits)
+    a, nxt, _ = eng.verify(0, d1)
+    _check(eng, a, nxt, ref, ra, rn, tol)
+
+    # block 2 from the same context: the oracle's greedy token after the
+    # pending one, then block 1's draft tokens (at least one token accepted)
+    eng.rollback(0, CTX, pending)
+    d2 = np.concatenate([[g1[0]], d1[1:]]).astype(np.int32)
+    print("[fullsize] oracle block 2", flush=True)
+    ref, ra, rn, tol = _oracle_block(shape, w, cache, pending, d2)
+    assert ra >= 1
+    a, nxt, _ = eng.verify(0, d2)
+    _check(eng, a, nxt, ref, ra, rn, tol)
+    assert eng.seq_state(0) == (CTX + 1 + a, nxt)
+
+
+def test_7b_speculative_stream_equals_greedy_loop_bitwise(model):
+    shape, _, eng = model
+    prompt = zipf_tokens(shape.vocab, CTX, seed=42)
+    eng.rollback(0, 0, -1)
+    first = eng.prefill(0, prompt)
+    target, rows = [first], []
+    for _ in range(80):
+        _, nxt, _ = eng.verify(0, [])
+        rows.append(eng.logits()[0].copy())
+        target.append(nxt)
+
+    # one block of the next 32 greedy tokens: every row equals the single-row
+    # block at its position bit for bit, and all 32 tokens are accepted
+    eng.rollback(0, CTX, first)
+    a, nxt, _ = eng.verify(0, target[1:K + 1])
+    assert (a, nxt) == (K, target[K + 1])
+    lg = eng.logits()
+    for t in range(K + 1):
+        assert np.array_equal(lg[t], rows[t]), f"row {t} differs from its single-row block"
+
+    # speculative steps with planted drafts of every accepted length
+    eng.rollback(0, CTX, first)
+    out = [first]
+    g = np.random.default_rng(3)
+    while len(out) < 40:
+        j = int(g.integers(0, K + 1))
+        d = planted_draft(target[len(out):], j, K, shape.vocab, seed=int(g.integers(1 << 30)))
+        a, nxt, _ = eng.verify(0, d)
+        assert a >= j   # a planted prefix is always accepted
+        out += list(d[:a]) + [nxt]
+    assert out == target[:len(out)]

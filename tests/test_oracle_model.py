@@ -207,3 +207,28 @@ def test_bf16_mode_rounds_cache_and_stays_near_unrounded():
     diff = np.abs(s.last_logits - exact.last_logits).max()
     # every bf16 rounding perturbs by at most 2^-9 relative
     assert 0 < diff < 0.02 * np.abs(exact.last_logits).max()
+
+
+def test_rounding_noise_probe_is_off_by_default_and_only_touches_bf16_rounding():
+    """The sensitivity probe leaves the definition alone: rel = 0 gives the
+    exact forward bit for bit, an fp32 model has no rounding points for it to
+    touch, and on a bf16 model a float32-sized error moves only values whose
+    operand sits within that error of a rounding boundary (a small, nonzero
+    change that a larger error makes larger)."""
+    toks = zipf_tokens(97, 24, seed=3)
+    depth, vis = chain_structure(len(toks))
+    for dt in ("f32", "bf16"):
+        shape = _small(dt)
+        w = gen_weights(shape, seed=4, std=0.2)
+        exact, _ = forward_block(shape, w, [], toks, depth, vis)
+        zero, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 0.0))
+        assert np.array_equal(exact, zero)
+        tiny, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 2.0 ** -23))
+        big, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 2.0 ** -12))
+        if dt == "f32":
+            assert np.array_equal(exact, tiny) and np.array_equal(exact, big)
+        else:
+            d_tiny = np.abs(tiny - exact).max()
+            d_big = np.abs(big - exact).max()
+            assert d_tiny < 0.05 * np.abs(exact).max()
+            assert d_tiny < d_big
