@@ -347,17 +347,23 @@ constexpr int RES_MAX_PARTS = 8;               // chunks per row (d <= 8192)
 
 // RMS scale of row t: 1 / sqrt(sum of its chunk sums, in chunk order, / d + eps).
 // The row's chunk sums come with two 16-byte loads.
-__device__ __forceinline__ float row_scale(const float* __restrict__ ssq, int t, int d, float eps) {
+struct RowSsq {
+  float4 a, b;   // chunk sums 0..7 of one row
+};
+__device__ __forceinline__ float row_scale_of(const RowSsq& r, int d, float eps) {
   static_assert(RES_MAX_PARTS == 8, "two 16-byte loads per row");
-  const float4 a = reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[0];
-  const float4 b = reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[1];
-  const float c[RES_MAX_PARTS] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  const float c[RES_MAX_PARTS] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
   const int np = (d + RES_COLS - 1) / RES_COLS;
   float s = c[0];
 #pragma unroll
   for (int i = 1; i < RES_MAX_PARTS; ++i)
     if (i < np) s += c[i];
   return 1.0f / sqrtf(s / (float)d + eps);
+}
+__device__ __forceinline__ float row_scale(const float* __restrict__ ssq, int t, int d, float eps) {
+  const RowSsq r{reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[0],
+                 reinterpret_cast<const float4*>(ssq + (size_t)t * RES_MAX_PARTS)[1]};
+  return row_scale_of(r, d, eps);
 }
 
 // ------------------------------------------------------ gate/up + SwiGLU --
@@ -404,11 +410,25 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   const bool rowl = MTV == 2 && T > 2 * 16;                  // the 33rd row, from LDS
   const int S = a.S;
   constexpr int NR = MTV == 2 ? 3 : 1;                       // reduced fragment tiles
-  constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
   const auto xs = make_rsrc(a.x, (unsigned)((size_t)((a.R + 15) / 16) * S * 1024));
   const auto ws = make_rsrc(a.w, (unsigned)((size_t)2 * a.n_pairs * S * 1024));
   __shared__ uint4 rowx[MTV == 2 ? SPW * GEMM_WAVES * 4 : 1];   // [super-step][grp]: the 33rd row
   __shared__ f32x4 red[2][GEMM_WAVES][NR][64];
+  // this thread's reduced item: fragment tile rm, lane rl (threads past NR * 64
+  // repeat an item and store nothing)
+  const int qq = threadIdx.x % (NR * 64);
+  const bool qown = threadIdx.x < NR * 64;
+  const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
+  // the chunk sums of the norm's row scale, requested first (memory counters
+  // complete in order) and used only in the epilogue
+  RowSsq rsq;
+  {
+    const auto sr = make_rsrc(a.ssq, (unsigned)((size_t)a.R * RES_MAX_PARTS * 4));
+    const unsigned so = qown && rt < T ? (unsigned)((row0 + rt) * RES_MAX_PARTS * 4) : OOB;
+    const uint4 u0 = bload<0>(sr, so), u1 = bload<0>(sr, so == OOB ? OOB : so + 16);
+    rsq.a = make_float4(__uint_as_float(u0.x), __uint_as_float(u0.y), __uint_as_float(u0.z), __uint_as_float(u0.w));
+    rsq.b = make_float4(__uint_as_float(u1.x), __uint_as_float(u1.y), __uint_as_float(u1.z), __uint_as_float(u1.w));
+  }
   uint4 xr[SPW][MTV];
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
@@ -418,13 +438,15 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
       xr[i][m] = bload<0>(xs, (sl < S && m * 16 + c < min(T, 2 * 16))
                                   ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
   }
-  if (MTV == 2) {
-    // every entry the MFMAs read is written: zeros past K or without a 33rd row
-    for (int it = threadIdx.x; it < SPW * GEMM_WAVES * 4; it += GEMM_WAVES * 64)
-      rowx[it] = bload<0>(xs, (rowl && (it >> 2) < S)
-                                  ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
-                                  : OOB);
-  }
+  // the 33rd row: thread it holds entry it of rowx ([super-step][grp]; at most
+  // one per thread, SPW <= 16); every entry the MFMAs read is written, zeros
+  // past K or without a 33rd row
+  static_assert(SPW * GEMM_WAVES * 4 <= GEMM_WAVES * 64, "one rowx entry per thread");
+  const int it = threadIdx.x;
+  const bool rowx_own = MTV == 2 && it < SPW * GEMM_WAVES * 4;
+  const uint4 rowv = bload<0>(xs, (rowx_own && rowl && (it >> 2) < S)
+                                      ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
+                                      : OOB);
   // tile k of this workgroup: pair g + (k / 2) P, gate (k even) or up (k odd)
   const int npair = g < a.n_pairs ? (a.n_pairs - g + a.P - 1) / a.P : 0;
   const int ntile = 2 * npair;
@@ -433,17 +455,16 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     const int sl = wv + GEMM_WAVES * i;
     return bload<2>(ws, (k < ntile && sl < S) ? (unsigned)(((tile_of(k) * S + sl) * 64 + lane) * 16) : OOB);
   };
-  __syncthreads();
-  // this thread's reduced item: fragment tile rm, lane rl (threads past NR * 64
-  // repeat an item and store nothing)
-  const int qq = threadIdx.x % (NR * 64);
-  const bool qown = threadIdx.x < NR * 64;
-  const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
-  const float rs = qown && rt < T ? row_scale(a.ssq, row0 + rt, a.d, a.eps) : 0.f;   // the norm's row scale
-  f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
+  // the first half tile of weights is requested before the 33rd row is
+  // stored: that store waits for every load issued before it (in order), so
+  // the weight stream starts with the input loads instead of after them
+  constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
   uint4 wa[HA], wb[HB > 0 ? HB : 1];
 #pragma unroll
   for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
+  if (rowx_own) rowx[it] = rowv;
+  __syncthreads();
+  f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < ntile; ++k) {
     f32x4 acc[NR];
 #pragma unroll
@@ -478,6 +499,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     } else if (qown && rt < T) {
       // features 16p + 4(rl / 16) .. +3 of row row0 + rt
       const int f = 16 * (g + (k >> 1) * a.P) + 4 * (rl >> 4);
+      const float rs = row_scale_of(rsq, a.d, a.eps);   // the norm's row scale
       float zv[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) zv[r] = silu_mul(gate[r] * rs, v[r] * rs);
