@@ -469,24 +469,36 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     f32x4 acc[NR];
 #pragma unroll
     for (int m = 0; m < NR; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto step = [&](const uint4& wf, int i) {
+    // the 33rd row's fragments are read from LDS RG super-steps at a time,
+    // ahead of their MFMAs (one wait per group, not one per super-step)
+    constexpr int RG = MTV == 2 ? 4 : (HA > 0 ? HA : 1);
+    auto steps = [&](const uint4* wf, int i0, int n) {
 #pragma unroll
-      for (int m = 0; m < MTV; ++m) acc[m] = mma<DT>(wf, xr[i][m], acc[m]);
-      if (MTV == 2) {
-        const uint4 r = rowx[(wv + GEMM_WAVES * i) * 4 + grp];
-        acc[2] = mma<DT>(wf, c == 0 ? r : make_uint4(0u, 0u, 0u, 0u), acc[2]);
+      for (int g0 = 0; g0 < n; g0 += RG) {
+        uint4 rv[RG];
+#pragma unroll
+        for (int j = 0; j < RG; ++j)
+          if (MTV == 2 && g0 + j < n) {
+            const uint4 r = rowx[(wv + GEMM_WAVES * (i0 + g0 + j)) * 4 + grp];
+            rv[j] = c == 0 ? r : make_uint4(0u, 0u, 0u, 0u);
+          }
+#pragma unroll
+        for (int j = 0; j < RG; ++j)
+          if (g0 + j < n) {
+#pragma unroll
+            for (int m = 0; m < MTV; ++m) acc[m] = mma<DT>(wf[g0 + j], xr[i0 + g0 + j][m], acc[m]);
+            if (MTV == 2) acc[2] = mma<DT>(wf[g0 + j], rv[j], acc[2]);
+          }
       }
     };
     // second half of this tile in flight while the first is multiplied, then
     // the first half of the next tile while the second is
 #pragma unroll
     for (int i = 0; i < HB; ++i) wb[i] = wload(k, HA + i);
-#pragma unroll
-    for (int i = 0; i < HA; ++i) step(wa[i], i);
+    steps(wa, 0, HA);
 #pragma unroll
     for (int i = 0; i < HA; ++i) wa[i] = wload(k + 1, i);
-#pragma unroll
-    for (int i = 0; i < HB; ++i) step(wb[i], HA + i);
+    steps(wb, HA, HB);
     const int pb = k & 1;
 #pragma unroll
     for (int m = 0; m < NR; ++m) red[pb][wv][m][lane] = acc[m];
