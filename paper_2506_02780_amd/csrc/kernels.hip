@@ -1380,7 +1380,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
 // order), so the two kernels give bitwise equal states; this one only avoids
 // staging the split again for every four query tiles.
 constexpr int WIDE_THREADS = 512;
-constexpr int WIDE_MIN_QT = 24;   // query tiles per sequence from which the wide kernel is used
+constexpr int WIDE_MIN_QT = 13;   // query tiles per sequence from which the wide kernel is used
 
 template <int DT, int HD>
 __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int nqg) {
