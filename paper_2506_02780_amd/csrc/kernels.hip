@@ -818,6 +818,11 @@ struct AttnArgs {
   int T, H, Hkv, G, ncols;  // T rows and ncols = T * G query columns per sequence
   int B;                    // sequences: rows b*T .. b*T + T - 1, columns b*ncols ..
   int tree;
+  // 0: every split of the grid; 1: only splits holding committed keys and the
+  // pending row alone (sp < (n + 1) / SPLIT; what every row of a draft tree
+  // sees unmasked); 2: the splits from (n + 1) / SPLIT on, grid y counted
+  // from there (a tree's own rows)
+  int split_mode;
   float scale_log2;         // log2(e) / sqrt(hd)
   float* part;              // [splits][Hkv][B * ncols][hd + 2]
   int max_pages;            // pages per layer in the pool
@@ -1069,7 +1074,8 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
 
   const int nqt = (a.ncols + 15) / 16;
   const int qgs = (nqt + ATT_QT - 1) / ATT_QT;   // query-tile groups per sequence
-  const int gkv = blockIdx.x, sp = blockIdx.y, b = blockIdx.z / qgs, qgrp = blockIdx.z % qgs;
+  const int gkv = blockIdx.x, b = blockIdx.z / qgs, qgrp = blockIdx.z % qgs;
+  int sp = blockIdx.y;
   // this sequence's rows, positions, paths, pages and step state
   const int rb = b * a.T;
   const int* pos = a.pos + rb;
@@ -1078,7 +1084,9 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   // (n, splits in use) with one vector load
   const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
   const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
+  if (a.split_mode == 2) sp += (n + 1) / SPLIT;
   if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
+  if (a.split_mode == 1 && sp >= (n + 1) / SPLIT) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, c = lane & 15;
   const int nkeys = n + a.T;            // slots written so far
@@ -1400,6 +1408,7 @@ __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int
   const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
   const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
   if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
+  if (a.split_mode == 1 && sp >= (n + 1) / SPLIT) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, c = lane & 15;
   const int nkeys = n + a.T;
@@ -2001,7 +2010,26 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if ((e = timed(prof, PC_ATTN, st, [&] {
            // KV head fastest (one head per XCD L2); ATT_QT query tiles per workgroup
            const int qt = att_qt(aa.tree);
-           if (!aa.tree && nqt >= WIDE_MIN_QT) {
+           const bool wide = nqt >= WIDE_MIN_QT;
+           if (aa.tree && wide) {
+             // a large tree: the splits below its rows hold keys every row sees
+             // unmasked, computed by the wide kernel; the tree kernel takes
+             // only the (at most two) splits holding the tree's rows
+             static_assert(64 + 1 <= SPLIT, "a tree (at most 64 nodes) spans at most two splits");
+             AttnArgs lin = aa;
+             lin.tree = 0;
+             lin.split_mode = 1;
+             const int per = m.Hkv * nsplit * B;
+             const int nqg = std::max(1, std::min((nqt + 7) / 8, (512 + per - 1) / per));
+             hipLaunchKernelGGL((attn_wide_kernel<DT, HD>), dim3(m.Hkv, nsplit, B * nqg), dim3(WIDE_THREADS), 0, st,
+                                lin, nqg);
+             AttnArgs tail = aa;
+             tail.split_mode = 2;
+             hipLaunchKernelGGL((attn_kernel<DT, HD, true>), dim3(m.Hkv, std::min(nsplit, 2), B * ((nqt + qt - 1) / qt)),
+                                dim3(att_threads(true)), 0, st, tail);
+             return last();
+           }
+           if (!aa.tree && wide) {
              // many query tiles: stage each split once per group of them; the
              // groups per sequence keep about two workgroups per CU in flight
              const int per = m.Hkv * nsplit * B;
