@@ -56,12 +56,15 @@ def _path_rows(parent, node):
     return [0] + rows[::-1]
 
 
-@pytest.mark.parametrize("cfg", ["tiny", "bf16"])
+@pytest.mark.parametrize("cfg", ["tiny", "bf16", "bf16_g4"])
 def test_tree_verify_matches_oracle(ee, cfg):
     if cfg == "tiny":
         shape, tol, std = get_shape("tiny"), 1e-4, 0.1
-    else:
+    elif cfg == "bf16":
         shape, tol, std = _bf16_small(), 2e-2, 0.02
+    else:
+        # 4 query heads per KV head: 64-node trees take the two-launch path
+        shape, tol, std = _bf16_small(d_model=1024, n_heads=8), 2e-2, 0.02
     w = gen_weights(shape, seed=41, std=std, gains="random")
     prompt = zipf_tokens(shape.vocab, 237, seed=12)     # blocks cross a 256-position split
     ref = OracleSession(shape, w)
@@ -103,9 +106,13 @@ def test_tree_verify_matches_oracle(ee, cfg):
     eng.close()
 
 
-@pytest.mark.parametrize("prompt_len", [150, 250])
-def test_tree_rows_equal_chain_rows_bitwise(ee, prompt_len):
-    shape = _bf16_small()
+@pytest.mark.parametrize("prompt_len,heads", [(150, 4), (250, 4), (150, 8), (255, 8), (300, 8)])
+def test_tree_rows_equal_chain_rows_bitwise(ee, prompt_len, heads):
+    # heads = 8 (4 query heads per KV head): the 64-node tree has 17 query
+    # tiles and runs as a wide launch over the splits below its rows plus the
+    # tree kernel over the splits holding them (from slot n + 1: split 0 at
+    # n = 150, split 1 at n = 255 and 300); the 40-node tree stays in one launch
+    shape = _bf16_small() if heads == 4 else _bf16_small(d_model=1024, n_heads=8)
     w = gen_weights(shape, seed=42, std=0.05)
     prompt = zipf_tokens(shape.vocab, prompt_len, seed=13)
     eng = ee.Engine(shape, w, max_ctx=640, k_max=64)
