@@ -56,11 +56,17 @@ def test_long_planted_drafts_accept_exactly(ee):
     eng.close()
 
 
-def test_long_block_rows_equal_short_block_rows_bitwise(ee):
+@pytest.mark.parametrize("width", [512, 4096])
+def test_long_block_rows_equal_short_block_rows_bitwise(ee, width):
     """Rows of a 401-row block equal the same rows computed one block at a
-    time (K = 0 steps) bit for bit: logits and the committed K/V."""
-    shape = _bf16_small()
-    w = gen_weights(shape, seed=92, std=0.05)
+    time (K = 0 steps) bit for bit: logits and the committed K/V.  Width 4096
+    (one layer): the projections run two K slices and the gate/up kernel a
+    single pass over d, in 32-row groups at 401 rows and one row alone."""
+    if width == 512:
+        shape = _bf16_small()
+    else:
+        shape = _bf16_small(n_layers=1, d_model=4096, n_heads=32, n_kv_heads=8, ffn=2048)
+    w = gen_weights(shape, seed=92, std=0.05 if width == 512 else 0.02)
     prompt = zipf_tokens(shape.vocab, 130, seed=4)
     eng = ee.Engine(shape, w, max_ctx=1024, k_max=512)
     eng.prefill(0, prompt)
