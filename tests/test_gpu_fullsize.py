@@ -16,9 +16,10 @@ committed context, replayed from captured graphs.
   evaluation that is not the exact one.
 * Properties that need no oracle, after a real 2048-token prefill: the
   speculative stream equals the GPU's own token-by-token greedy loop bit for
-  bit (the lossless property of greedy verification, Eq. 7), and the rows of a
+  bit (the lossless property of greedy verification, Eq. 7), the rows of a
   33-row block carry bitwise the logits of the single-row blocks at the same
-  positions.
+  positions, and the rows of a 64-node draft tree those of the linear chains
+  along their paths.
 """
 
 import numpy as np
@@ -47,7 +48,7 @@ def model(ee):
     shape = get_shape("7b")
     print(f"[fullsize] drawing {shape.name} weights", flush=True)
     w = gen_weights(shape, seed=1234)
-    eng = ee.Engine(shape, w, max_ctx=CTX + 128, k_max=K)
+    eng = ee.Engine(shape, w, max_ctx=CTX + 128, k_max=64)
     yield shape, w, eng
     eng.close()
 
@@ -134,3 +135,39 @@ def test_7b_speculative_stream_equals_greedy_loop_bitwise(model):
         assert a >= j   # a planted prefix is always accepted
         out += list(d[:a]) + [nxt]
     assert out == target[:len(out)]
+
+
+def test_7b_tree_rows_equal_chain_rows_bitwise(model):
+    """A 64-node tree (depth 8, branching 3) over the 2048-token prefill, the
+    benchmark's tree configuration (17 query tiles: the committed splits
+    through the wide kernel, the tree's own split through the tree kernel):
+    every row of the tree equals, bit for bit, the same token path verified
+    as a linear chain, and the accepted path commits the chain's cache."""
+    from workloads import random_tree, tree_tokens
+    shape, _, eng = model
+    prompt = zipf_tokens(shape.vocab, CTX, seed=43)
+    eng.rollback(0, 0, -1)
+    first = eng.prefill(0, prompt)
+    truth = [eng.verify(0, [])[1] for _ in range(9)]
+    parent = random_tree(64, max_depth=8, max_branch=3, seed=17)
+    toks = tree_tokens(parent, truth[:5], shape.vocab, seed=17)
+    eng.rollback(0, CTX, first)
+    a, nxt, nodes = eng.verify(0, toks, parent)
+    assert a >= 5   # the first-child chain follows the greedy continuation
+    tree_lg = eng.logits()
+    tree_kv = eng.read_kv(0, shape.n_layers - 1)
+    leaves = sorted(set(range(64)) - set(int(p) for p in parent))
+    g = np.random.default_rng(5)
+    for leaf in [int(nodes[-1])] + [int(x) for x in g.choice(leaves, 2, replace=False)]:
+        rows, node = [], leaf
+        while node >= 0:
+            rows.append(node + 1)
+            node = int(parent[node])
+        rows = [0] + rows[::-1]
+        eng.rollback(0, CTX, first)
+        ca, cn, _ = eng.verify(0, toks[np.asarray(rows[1:], dtype=np.int64) - 1])
+        assert np.array_equal(eng.logits(), tree_lg[rows])
+        if leaf == int(nodes[-1]):
+            assert (ca, cn) == (a, nxt)
+            ck, cv = eng.read_kv(0, shape.n_layers - 1)
+            assert np.array_equal(ck, tree_kv[0]) and np.array_equal(cv, tree_kv[1])
