@@ -362,6 +362,18 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
   return &slot;
 }
 
+// Order the context's stream after the work enqueued on the caller's stream.
+// An idle caller stream (the usual case) needs no event, whose record and wait
+// cost ~15 us of host time per call.
+int order_after_user(ee_ctx* c) {
+  const hipError_t q = hipStreamQuery(c->user_st);
+  if (q == hipSuccess) return EE_OK;
+  if (q != hipErrorNotReady) return hip_fail(c, q, "hipStreamQuery");
+  HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
+  HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
+  return EE_OK;
+}
+
 // Stage the per-sequence state (page tables, committed lengths, the KV slot
 // of every row) in the pinned mirror, run the block of B sequences of T rows
 // whose tokens, positions and parents the caller staged (its kernels read the
@@ -385,14 +397,8 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
       slot[b * T + t] = s.pages[p / PAGE] * PAGE + p % PAGE;
     }
   }
-  // order the block after the caller's stream; an idle stream (the usual case)
-  // needs no event, whose record and wait cost ~15 us of host time per call
-  const hipError_t q = hipStreamQuery(c->user_st);
-  if (q != hipSuccess) {
-    if (q != hipErrorNotReady) return hip_fail(c, q, "hipStreamQuery");
-    HIP_TRY(c, hipEventRecord(c->ev_user, c->user_st));
-    HIP_TRY(c, hipStreamWaitEvent(c->st, c->ev_user, 0));
-  }
+  int rc = order_after_user(c);
+  if (rc) return rc;
   const ee::Step step{T, B, mode};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
@@ -914,6 +920,7 @@ int32_t ee_load_kv(ee_ctx* c, int32_t seq, int32_t n, int32_t pending, const voi
   Seq& s = c->seqs[seq];
   if (s.live) return fail(c, EE_ESTATE, "sequence already holds tokens (roll it back to 0 first)");
   if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "cache longer than max_ctx - 1");
+  if ((rc = order_after_user(c))) return rc;
   int added;
   if (!reserve_pages(c, s, n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
   const size_t esz = c->cfg.dtype == EE_BF16 ? 2 : 4;
