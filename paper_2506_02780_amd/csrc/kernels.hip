@@ -435,8 +435,9 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     const int sl = wv + GEMM_WAVES * i;
 #pragma unroll
     for (int m = 0; m < MTV; ++m)
-      xr[i][m] = bload<0>(xs, (sl < S && m * 16 + c < min(T, 2 * 16))
-                                  ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
+      if (MTV == 2)   // (one register tile: requested with the first weights below)
+        xr[i][m] = bload<0>(xs, (sl < S && m * 16 + c < min(T, 2 * 16))
+                                    ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
   }
   // the 33rd row: thread it holds entry it of rowx ([super-step][grp]; at most
   // one per thread, SPW <= 16); every entry the MFMAs read is written, zeros
@@ -460,8 +461,20 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   // the weight stream starts with the input loads instead of after them
   constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
   uint4 wa[HA], wb[HB > 0 ? HB : 1];
+  if (MTV == 1) {
+    // one register tile: inputs and the first half tile of weights requested
+    // super-step by super-step, in the order the first MFMAs use them
 #pragma unroll
-  for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
+    for (int i = 0; i < SPW; ++i) {
+      const int sl = wv + GEMM_WAVES * i;
+      xr[i][0] = bload<0>(xs, (sl < S && c < T) ? (unsigned)((((row0 / 16) * S + sl) * 64 + lane) * 16) : OOB);
+      if (i < HA) wa[i] = wload(0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
+  }
   if (rowx_own) rowx[it] = rowv;
   __syncthreads();
   f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
