@@ -213,8 +213,9 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
     const int sl = wv + GEMM_WAVES * i;
 #pragma unroll
     for (int m = 0; m < MT; ++m)
-      xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < T)
-                                  ? (unsigned)(((m * S + s0 + sl) * 64 + lane) * 16) : OOB);
+      if (MT > 1)   // (one tile: requested with the first weights below)
+        xr[i][m] = bload<0>(xs, (sl < ns && m * 16 + c < T)
+                                    ? (unsigned)(((m * S + s0 + sl) * 64 + lane) * 16) : OOB);
   }
   auto wload = [&](int tl, int i) {
     const int sl = wv + GEMM_WAVES * i;
@@ -250,8 +251,20 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_kernel(GemmArgs a) {
   // the current tile is computed, and no in-flight register is ever copied
   int tile = q / a.SK;
   uint4 wa[GEMM_SPW], wb[GEMM_SPW];
+  if (MT == 1) {
+    // one row tile: inputs and the first tile's weights requested super-step
+    // by super-step, in the order the first MFMAs use them
 #pragma unroll
-  for (int i = 0; i < GEMM_SPW; ++i) wa[i] = wload(tile, i);
+    for (int i = 0; i < GEMM_SPW; ++i) {
+      const int sl = wv + GEMM_WAVES * i;
+      xr[i][0] = bload<0>(xs, (sl < ns && c < T) ? (unsigned)(((s0 + sl) * 64 + lane) * 16) : OOB);
+      wa[i] = wload(tile, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < GEMM_SPW; ++i) wa[i] = wload(tile, i);
+  }
   for (;;) {
 #pragma unroll
     for (int i = 0; i < GEMM_SPW; ++i) wb[i] = wload(tile + groups, i);
