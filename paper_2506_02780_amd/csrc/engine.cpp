@@ -186,7 +186,8 @@ struct ee_ctx {
     hipGraphExec_t exec;
     int prof_pairs;                  // event pairs recorded by the graph's own nodes
   };
-  std::map<std::tuple<int, int, int, uint32_t>, Captured> graphs;   // (T, B, mode, profiling mask)
+  // (T, B, mode, attention splits, profiling mask)
+  std::map<std::tuple<int, int, int, int, uint32_t>, Captured> graphs;
   bool graphs_ok = true;             // capture works on this stream
   bool graphs_on = true;             // ee_use_graphs
   unsigned char* packed = nullptr;
@@ -332,14 +333,24 @@ hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
   return ee::run_result_out(c->w, step.B, c->d_result_dst, c->st);
 }
 
-// Captured graph of a (T, mode) block shape, built on first use (profiling
-// events, when enabled, become event-record nodes of the graph); nullptr if
-// capture is unavailable (the block then runs eagerly).
+constexpr size_t MAX_GRAPHS = 512;   // captured block shapes kept at once
+
+// Captured graph of a (T, B, mode, splits) block shape, built on first use
+// (profiling events, when enabled, become event-record nodes of the graph);
+// nullptr if capture is unavailable (the block then runs eagerly).  The
+// attention grid is sized to the block's splits, so a context that grows
+// past a multiple of 256 positions captures the shape again; past MAX_GRAPHS
+// shapes the cache starts over (every call waits for its graph, so none is
+// in flight).
 const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
   if (!c->graphs_ok || !c->graphs_on) return nullptr;
-  const auto key = std::make_tuple(step.T, step.B, step.mode, prof ? prof->mask : 0u);
+  const auto key = std::make_tuple(step.T, step.B, step.mode, step.splits, prof ? prof->mask : 0u);
   auto it = c->graphs.find(key);
   if (it != c->graphs.end()) return &it->second;
+  if (c->graphs.size() >= MAX_GRAPHS) {
+    for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second.exec);
+    c->graphs.clear();
+  }
   hipGraph_t g = nullptr;
   hipGraphExec_t ge = nullptr;
   if (hipStreamBeginCapture(c->st, hipStreamCaptureModeThreadLocal) != hipSuccess) {
@@ -385,11 +396,13 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
   int* info = reinterpret_cast<int*>(c->h_stage + L.s_info);
   int* slot = reinterpret_cast<int*>(c->h_stage + L.s_slot);
+  int splits = 1;
   for (int b = 0; b < B; ++b) {
     const Seq& s = *seqs[b];
     for (size_t i = 0; i < s.pages.size(); ++i) ptab[b * L.ptable_len + i] = s.pages[i];
     info[4 * b + 0] = s.len;
     info[4 * b + 1] = (s.len + T + SPLIT - 1) / SPLIT;
+    splits = std::max(splits, info[4 * b + 1]);
     info[4 * b + 2] = top_k;
     info[4 * b + 3] = dynamic;
     for (int t = 0; t < T; ++t) {
@@ -399,7 +412,7 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
   }
   int rc = order_after_user(c);
   if (rc) return rc;
-  const ee::Step step{T, B, mode};
+  const ee::Step step{T, B, mode, splits};
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
   const ee_ctx::Captured* cg = prof ? nullptr : block_graph(c, step, nullptr);

@@ -112,6 +112,8 @@ struct Step {
   int B;        // sequences in the block
   int mode;     // 0 prefill, 1 linear verify, 2 tree verify, 3 linear top-k verify,
                 // 4 linear stochastic verify (one sequence)
+  int splits;   // attention splits of the grid: the most any sequence of the
+                // block uses, ceil((n + T) / 256); 1 .. max_splits
 };
 
 enum ProfClass {

@@ -1517,8 +1517,8 @@ constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 
 // Merge the splits of every (row, head) in split order; write the attention
 // output as packed activations of the O projection.  4 dims per thread.  The
-// state of every split the grid may have written (max_splits, fixed at launch)
-// is fetched in one batch; only the first info[1] take part.
+// state of every split of the attention grid (max_splits, fixed at launch) is
+// fetched in one batch; only the first info[1] of the row's sequence take part.
 template <int DT, int HD>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
                                                               const int* __restrict__ info, int max_splits,
@@ -2007,7 +2007,10 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     return e;
 
   const int G = m.H / m.Hkv, ncols = T * G;   // query columns per sequence
-  const int nsplit = w.max_splits;   // splits beyond the context exit at once
+  // the grid covers the splits of the block's longest context; a shorter
+  // sequence's splits beyond its own exit at once
+  const int nsplit = s.splits;
+  if (nsplit < 1 || nsplit > w.max_splits || nsplit > MAX_SPLITS) return hipErrorInvalidValue;
   const int nqt = (ncols + 15) / 16;
   const int pairs = (m.H + 2 * m.Hkv) * (m.hd / 2);
 
@@ -2075,7 +2078,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     if ((e = timed(prof, PC_COMBINE, st, [&] {
            hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3((R * m.H + 1024 / HD - 1) / (1024 / HD)), dim3(256), 0,
                               st, w.attn_part,
-                              w.info, w.max_splits, m.Hkv, G, R * G, m.H, T, (void*)w.xbuf, Sq);
+                              w.info, nsplit, m.Hkv, G, R * G, m.H, T, (void*)w.xbuf, Sq);
            return last();
          })) != hipSuccess)
       return e;
