@@ -302,8 +302,10 @@ int32_t ee_load_kv(ee_ctx* ctx, int32_t seq, int32_t n, int32_t pending, const v
                    const void* host_v);
 
 /* Launch mode of later prefill/verify blocks.  on != 0 (the default): the
- * kernels of each block shape (row count, linear/tree/prefill) are captured
- * once into a HIP graph and replayed; on == 0: every kernel is launched
+ * kernels of each block shape (row count, sequences, linear/tree/prefill, and
+ * the attention splits of the longest context, ceil((n + T) / 256)) are
+ * captured once into a HIP graph and replayed (at most 512 shapes are kept;
+ * past that the cache starts over); on == 0: every kernel is launched
  * individually.  Both run the same kernels with the same arguments. */
 int32_t ee_use_graphs(ee_ctx* ctx, int32_t on);
 

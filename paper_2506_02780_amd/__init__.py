@@ -336,7 +336,8 @@ class Engine:
         _check(ee_load_kv(self.ctx, seq, k.shape[1], int(pending), k.ctypes.data, v.ctypes.data), self.ctx)
 
     def use_graphs(self, on: bool):
-        """Replay captured HIP graphs per block shape (default) or launch eagerly."""
+        """Replay captured HIP graphs per block shape and attention split count
+        (default) or launch eagerly."""
         _check(ee_use_graphs(self.ctx, int(bool(on))), self.ctx)
 
     def profile(self, classes=()):

@@ -100,3 +100,35 @@ def test_graph_replays_equal_eager_launches(ee):
         np.testing.assert_array_equal(eng.logits(), ref_logits)
         del x
     eng.close()
+
+
+def test_graphs_per_split_count_equal_eager_launches(ee):
+    """The attention grid covers the splits of the block's context (256
+    positions each), so a block shape is captured once per split count:
+    contexts on both sides of split boundaries give, from their graphs, the
+    eager result bitwise, also when a shape is replayed after others."""
+    shape = get_shape("tiny", n_layers=2, d_model=512, n_heads=4, n_kv_heads=2, head_dim=128,
+                      ffn=1024, vocab=2048, dtype="bf16")
+    w = gen_weights(shape, seed=9, std=0.05)
+    prompt = zipf_tokens(shape.vocab, 700, seed=5)
+    draft = zipf_tokens(shape.vocab, 20, seed=6)
+    eng = ee.Engine(shape, w, max_ctx=1024, k_max=32)
+    ctxs = (100, 235, 236, 511, 600)   # n + 21 rows: 1, 1, 2, 3, 3 splits
+
+    def at(n):
+        # the prompt's first n tokens committed, its next token pending
+        eng.rollback(0, 0, -1)
+        eng.prefill(0, prompt)
+        eng.rollback(0, n, int(prompt[n]))
+
+    ref = {}
+    eng.use_graphs(False)
+    for n in ctxs:
+        at(n)
+        ref[n] = (eng.verify(0, draft)[:2], eng.logits())
+    eng.use_graphs(True)
+    for n in ctxs + ctxs[::-1]:
+        at(n)
+        assert eng.verify(0, draft)[:2] == ref[n][0]
+        np.testing.assert_array_equal(eng.logits(), ref[n][1])
+    eng.close()
