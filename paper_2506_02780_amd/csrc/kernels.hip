@@ -1519,16 +1519,18 @@ constexpr int MAX_SPLITS = 32;   // committed + block positions <= 8192
 // output as packed activations of the O projection.  4 dims per thread.  The
 // state of every split of the attention grid (max_splits, fixed at launch) is
 // fetched in one batch; only the first info[1] of the row's sequence take part.
+constexpr int CMB_THREADS = 128;   // 4 (row, head) columns per workgroup at head_dim 128
+
 template <int DT, int HD>
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
+__global__ __launch_bounds__(CMB_THREADS) void attn_combine_kernel(const float* __restrict__ part,
                                                               const int* __restrict__ info, int max_splits,
                                                               int Hkv, int G, int ncols, int H, int T,
                                                               void* __restrict__ xout, int x_S) {
   // ncols: query columns of the whole block (all sequences); row t belongs to
   // sequence t / T
-  // 1024 / HD (row, head) columns per workgroup, HD / 4 threads of 4 dims each
+  // CMB_THREADS * 4 / HD (row, head) columns per workgroup, HD / 4 threads of 4 dims each
   constexpr int TPC = HD / 4;
-  const int pq = blockIdx.x * (256 / TPC) + threadIdx.x / TPC;
+  const int pq = blockIdx.x * (CMB_THREADS / TPC) + threadIdx.x / TPC;
   if (pq >= ncols / G * H) return;
   const int t = pq / H, j = pq % H;
   const int gkv = j / G, qc = t * G + (j % G);
@@ -2076,7 +2078,9 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_COMBINE, st, [&] {
-           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3((R * m.H + 1024 / HD - 1) / (1024 / HD)), dim3(256), 0,
+           constexpr int per_wg = CMB_THREADS * 4 / HD;   // (row, head) columns per workgroup
+           static_assert(per_wg >= 1, "one column per workgroup at least");
+           hipLaunchKernelGGL((attn_combine_kernel<DT, HD>), dim3((R * m.H + per_wg - 1) / per_wg), dim3(CMB_THREADS), 0,
                               st, w.attn_part,
                               w.info, nsplit, m.Hkv, G, R * G, m.H, T, (void*)w.xbuf, Sq);
            return last();
