@@ -24,9 +24,19 @@ decoder-only code LLMs; its text does not spell the layers out):
     logits = (RMSNorm(h) * g_final) Wlm^T
 
 Everything is float64.  For bf16 models, the quantities a bf16 pipeline
-stores in bf16 are rounded to bf16 (nearest-even): the inputs of the
-projections that follow a norm, q and k after RoPE, v (so the cache holds
-bf16 keys and values), the attention output o and the SwiGLU product.
+stores in bf16 are rounded to bf16 (nearest-even); the paper states no
+precision, so these rounding sites are this implementation's reading of one
+(the list is fixed; a kernel is checked against it, it does not follow a
+kernel):
+
+    x_attn   h * g_attn, the input of the q/k/v projections
+    q, k     after RoPE (so the cache holds bf16 keys)
+    v        the value projection (the cache holds bf16 values)
+    o        the attention output, the input of the O projection
+    x_ffn    h * g_ffn, the input of the gate/up projections
+    z        silu(gate) * up, the input of the down projection
+    x_final  h * g_final, the input of the LM head
+
 Residual stream, scores, softmax and logits stay float64.  fp32 models are
 not rounded at all.
 
@@ -41,10 +51,6 @@ from __future__ import annotations
 import numpy as np
 
 from .numerics import round_bf16, to_f64
-
-
-def _rounder(dtype: str):
-    return round_bf16 if dtype == "bf16" else (lambda a: a)
 
 
 def rmsnorm(h, gain, eps):
@@ -120,7 +126,10 @@ def tree_structure(parent):
     return depth, vis
 
 
-def forward_block(shape, weights, cache, tokens, depth, vis, rounding_noise=None):
+ROUNDING_SITES = ("x_attn", "q", "k", "v", "o", "x_ffn", "z", "x_final")
+
+
+def forward_block(shape, weights, cache, tokens, depth, vis, rounding=None):
     """One forward of the target model over a block.
 
     shape   : model shape (n_layers, d_model, n_heads, n_kv_heads, head_dim,
@@ -130,24 +139,24 @@ def forward_block(shape, weights, cache, tokens, depth, vis, rounding_noise=None
               in the model dtype, logical [out, in] layout
     cache   : list per layer of (K, V), float64 [n, Hkv, hd] (already rounded)
     tokens  : [T] token ids; depth: [T]; vis: [T, T] bool
-    rounding_noise : None (the definition above) or (generator, rel), a
-              sensitivity probe for tests: every value rounded to bf16 is first
-              multiplied by 1 + rel * N(0, 1), an error of the size a float32
-              evaluation of the same expression carries.  The spread this
-              causes in the logits is the part of a bf16 pipeline's result that
-              its rounding points leave open (an operand within float32 error of
-              a rounding boundary may round either way).
+    rounding: None (the definition above), or a test hook called at every
+              rounding site of a bf16 model as rounding(site, layer, exact,
+              rounded) with the site name (ROUNDING_SITES), the layer (n_layers
+              for x_final), the exact float64 value and its bf16 rounding; the
+              forward continues with what it returns.  Tests use it to probe
+              the sensitivity to rounding flips, to drop one site, and to
+              follow another evaluation's choice where a value lies so close
+              to a bf16 rounding boundary that both neighbours are correct.
     Returns (logits [T, vocab] float64, block_kv: list per layer of (k, v) [T, Hkv, hd]).
     """
     dt = shape.dtype
-    rnd = _rounder(dt)
-    if rounding_noise is not None and dt == "bf16":
-        gen, rel = rounding_noise
-        exact = rnd
 
-        def rnd(a):
-            a = np.asarray(a, dtype=np.float64)
-            return exact(a * (1.0 + rel * gen.standard_normal(a.shape)))
+    def rnd(site, layer, a):
+        if dt != "bf16":
+            return a
+        r = round_bf16(a)
+        return r if rounding is None else rounding(site, layer, a, r)
+
     H, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     tokens = np.asarray(tokens, dtype=np.int64)
     t = len(tokens)
@@ -161,24 +170,24 @@ def forward_block(shape, weights, cache, tokens, depth, vis, rounding_noise=None
     block_kv = []
     for l in range(shape.n_layers):
         lw = weights.layer(l)
-        x = rnd(h * lw["attn_gain"].astype(np.float64))      # RMSNorm(h) * g = r * (h * g)
+        x = rnd("x_attn", l, h * lw["attn_gain"].astype(np.float64))   # RMSNorm(h) * g = r * (h * g)
         r = norm_scale(h, shape.rms_eps)
         q = ((x @ to_f64(lw["wq"], dt).T) * r).reshape(t, H, hd)
         k = ((x @ to_f64(lw["wk"], dt).T) * r).reshape(t, Hkv, hd)
         v = ((x @ to_f64(lw["wv"], dt).T) * r).reshape(t, Hkv, hd)
-        q = rnd(rope(q, pos, shape.rope_theta))
-        k = rnd(rope(k, pos, shape.rope_theta))
-        v = rnd(v)
+        q = rnd("q", l, rope(q, pos, shape.rope_theta))
+        k = rnd("k", l, rope(k, pos, shape.rope_theta))
+        v = rnd("v", l, v)
         block_kv.append((k, v))
         kc, vc = cache[l] if cache else (np.zeros((0, Hkv, hd)), np.zeros((0, Hkv, hd)))
         keys = np.concatenate([kc, k], axis=0)          # [n + T, Hkv, hd]
         vals = np.concatenate([vc, v], axis=0)
-        o = rnd(attention(q, keys, vals, mask, scale).reshape(t, H * hd))
+        o = rnd("o", l, attention(q, keys, vals, mask, scale).reshape(t, H * hd))
         h = h + o @ to_f64(lw["wo"], dt).T
-        x = rnd(h * lw["ffn_gain"].astype(np.float64))
+        x = rnd("x_ffn", l, h * lw["ffn_gain"].astype(np.float64))
         r = norm_scale(h, shape.rms_eps)
-        z = rnd(silu((x @ to_f64(lw["w_gate"], dt).T) * r) * ((x @ to_f64(lw["w_up"], dt).T) * r))
+        z = rnd("z", l, silu((x @ to_f64(lw["w_gate"], dt).T) * r) * ((x @ to_f64(lw["w_up"], dt).T) * r))
         h = h + z @ to_f64(lw["w_down"], dt).T
-    f = rnd(h * weights.final_gain.astype(np.float64))
+    f = rnd("x_final", shape.n_layers, h * weights.final_gain.astype(np.float64))
     logits = (f @ to_f64(weights.lm_head, dt).T) * norm_scale(h, shape.rms_eps)
     return logits, block_kv

@@ -28,11 +28,11 @@ from .model import chain_structure, forward_block, tree_structure
 
 
 class OracleSession:
-    def __init__(self, shape, weights, rounding_noise=None):
-        """rounding_noise: None, or (generator, rel) for forward_block's
-        sensitivity probe (tests only; None is the definition)."""
+    def __init__(self, shape, weights, rounding=None):
+        """rounding: None (the definition), or forward_block's rounding-site
+        test hook, used by every forward of the session."""
         self.shape, self.weights = shape, weights
-        self.rounding_noise = rounding_noise
+        self.rounding = rounding
         hk, hd = shape.n_kv_heads, shape.head_dim
         self.cache = [(np.zeros((0, hk, hd)), np.zeros((0, hk, hd))) for _ in range(shape.n_layers)]
         self.pending = None
@@ -55,7 +55,7 @@ class OracleSession:
     def prefill(self, tokens):
         tokens = np.asarray(tokens, dtype=np.int64)
         depth, vis = chain_structure(len(tokens))
-        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding_noise)
+        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding)
         self._commit(blk, np.arange(len(tokens)))
         self.pending = int(greedy_rows(logits[-1:])[0])
         self.last_logits = logits
@@ -71,7 +71,7 @@ class OracleSession:
             depth, vis = chain_structure(len(tokens))
         else:
             depth, vis = tree_structure(parent)
-        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding_noise)
+        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding)
         g = greedy_rows(logits)
         if parent is None:
             a, nxt = accept_linear(draft, g)
@@ -89,7 +89,7 @@ class OracleSession:
         pending and is returned."""
         rows = np.concatenate([[self.pending], np.asarray(tokens, dtype=np.int64)])
         depth, vis = chain_structure(len(rows))
-        logits, blk = forward_block(self.shape, self.weights, self.cache, rows, depth, vis, self.rounding_noise)
+        logits, blk = forward_block(self.shape, self.weights, self.cache, rows, depth, vis, self.rounding)
         self._commit(blk, np.arange(len(rows)))
         self.pending = int(greedy_rows(logits[-1:])[0])
         self.last_logits = logits
@@ -99,7 +99,7 @@ class OracleSession:
         """Logits of the chain [pending, d_1..d_K]; the cache is unchanged."""
         tokens = np.concatenate([[self.pending], np.asarray(draft, dtype=np.int64)])
         depth, vis = chain_structure(len(tokens))
-        logits, _ = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding_noise)
+        logits, _ = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding)
         return logits
 
     def verify_topk(self, draft, k: int, dynamic: bool = True):
@@ -110,7 +110,7 @@ class OracleSession:
         draft = np.asarray(draft, dtype=np.int64)
         tokens = np.concatenate([[self.pending], draft])
         depth, vis = chain_structure(len(tokens))
-        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding_noise)
+        logits, blk = forward_block(self.shape, self.weights, self.cache, tokens, depth, vis, self.rounding)
         a, nxt, taus = accept_topk(draft, logits, k, dynamic)
         self._commit(blk, list(range(a + 1)))
         self.pending = nxt

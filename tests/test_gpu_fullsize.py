@@ -1,19 +1,19 @@
-"""Full-size checks in the configuration the benchmark times: the 7B-class
+"""Full-depth checks in the configuration the benchmark times: the 7B-class
 bf16 decoder (32 layers, d_model 4096, 32 query / 8 KV heads, FFN 11008,
 vocab 32256), verify blocks of T = 33 rows (K = 32) over a 2048-position
 committed context, replayed from captured graphs.
 
-* Parity with the oracle: the committed context is a seeded random bf16 cache
-  installed on both sides (``ee_load_kv`` / ``OracleSession.set_cache``), so
-  the oracle needs no 2048-token prefill.  Two verify blocks are compared:
-  every logit of all 33 rows, and the acceptance exact wherever the oracle's
-  top-2 margins decide it.  The bound is max-abs 2e-2 or, where larger, twice
-  the oracle's own spread: the largest logit change of the oracle when each
-  value it rounds to bf16 carries a float32-sized relative error (2^-23
-  N(0, 1)).  At this depth that spread is ~0.12: an operand within float32
-  error of a bf16 rounding boundary rounds either way, and 32 layers of such
-  flips move the logits of this random model by ~9% of their spread, for any
-  evaluation that is not the exact one.
+* A supplementary sensitivity check against the oracle at full depth (the
+  stated 2e-2 is checked at full width one layer at a time in
+  test_gpu_fullwidth.py, where every rounding decision is checked too): the
+  committed context is a seeded random bf16 cache installed on both sides
+  (``ee_load_kv`` / ``OracleSession.set_cache``).  Through 32 layers a single
+  bf16 rounding flip (an operand within float32 error of a rounding
+  boundary) cascades through the later rounding sites, so any evaluation
+  that is not the exact one, the oracle itself with a float32-sized error at
+  its rounding sites included, moves the logits by ~0.12.  The GPU's error is
+  bounded here by max(2e-2, twice that spread, measured on the same inputs),
+  and the acceptance compared exactly wherever the oracle's margins exceed it.
 * Properties that need no oracle, after a real 2048-token prefill: the
   speculative stream equals the GPU's own token-by-token greedy loop bit for
   bit (the lossless property of greedy verification, Eq. 7), the rows of a
@@ -25,7 +25,7 @@ committed context, replayed from captured graphs.
 import numpy as np
 import pytest
 
-from helpers import assert_step_matches
+from helpers import assert_step_matches, noise_probe
 from oracle import OracleSession, greedy_rows
 from oracle.numerics import to_f64
 from workloads import gen_weights, get_shape, planted_draft, random_kv_context, zipf_tokens
@@ -60,7 +60,7 @@ def _oracle_block(shape, w, cache, pending, draft):
     ref = OracleSession(shape, w)
     ref.set_cache(cache, pending)
     ra, rn, _ = ref.verify(draft)
-    probe = OracleSession(shape, w, rounding_noise=(np.random.default_rng(7), NOISE))
+    probe = OracleSession(shape, w, rounding=noise_probe(np.random.default_rng(7), NOISE))
     probe.set_cache(cache, pending)
     probe.verify(draft)
     spread = float(np.abs(probe.last_logits - ref.last_logits).max())

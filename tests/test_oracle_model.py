@@ -209,25 +209,31 @@ def test_bf16_mode_rounds_cache_and_stays_near_unrounded():
     assert 0 < diff < 0.02 * np.abs(exact.last_logits).max()
 
 
-def test_rounding_noise_probe_is_off_by_default_and_only_touches_bf16_rounding():
-    """The sensitivity probe leaves the definition alone: rel = 0 gives the
-    exact forward bit for bit, an fp32 model has no rounding points for it to
-    touch, and on a bf16 model a float32-sized error moves only values whose
-    operand sits within that error of a rounding boundary (a small, nonzero
-    change that a larger error makes larger)."""
+def test_rounding_hook_is_off_by_default_and_only_sees_bf16_sites():
+    """The rounding-site hook leaves the definition alone: a hook that returns
+    the definition's rounding gives the same forward bit for bit, an fp32
+    model has no rounding sites for it to see, and on a bf16 model the noise
+    probe with a float32-sized error moves the logits a little (an operand
+    within that error of a rounding boundary rounds the other way) and a
+    larger error more."""
+    from tests.helpers import noise_probe
     toks = zipf_tokens(97, 24, seed=3)
     depth, vis = chain_structure(len(toks))
     for dt in ("f32", "bf16"):
         shape = _small(dt)
         w = gen_weights(shape, seed=4, std=0.2)
         exact, _ = forward_block(shape, w, [], toks, depth, vis)
-        zero, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 0.0))
-        assert np.array_equal(exact, zero)
-        tiny, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 2.0 ** -23))
-        big, _ = forward_block(shape, w, [], toks, depth, vis, (np.random.default_rng(1), 2.0 ** -12))
+        seen = []
+        same, _ = forward_block(shape, w, [], toks, depth, vis,
+                                rounding=lambda s, l, e, r: (seen.append((s, l)), r)[1])
+        assert np.array_equal(exact, same)
+        tiny, _ = forward_block(shape, w, [], toks, depth, vis, noise_probe(np.random.default_rng(1), 2.0 ** -23))
+        big, _ = forward_block(shape, w, [], toks, depth, vis, noise_probe(np.random.default_rng(1), 2.0 ** -12))
         if dt == "f32":
+            assert seen == []
             assert np.array_equal(exact, tiny) and np.array_equal(exact, big)
         else:
+            assert len(seen) == 7 * shape.n_layers + 1
             d_tiny = np.abs(tiny - exact).max()
             d_big = np.abs(big - exact).max()
             assert d_tiny < 0.05 * np.abs(exact).max()
