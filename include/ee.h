@@ -301,6 +301,33 @@ int32_t ee_read_kv(ee_ctx* ctx, int32_t seq, int32_t layer, void* host_k, void* 
 int32_t ee_load_kv(ee_ctx* ctx, int32_t seq, int32_t n, int32_t pending, const void* host_k,
                    const void* host_v);
 
+/* Bytes of the capture buffer ee_capture needs for blocks of `rows` rows
+ * (all sequences of the block together), or 0 for an invalid config or
+ * rows < 1.  With R = rows, R16 = R rounded up to a multiple of 16, E = 2
+ * (bf16) or 4 (fp32), qd = n_heads * head_dim and kd = n_kv_heads * head_dim,
+ * every layer takes E * (R16 * (2 d_model + qd + ffn) + R * (qd + 2 kd))
+ * bytes and the LM head's input E * R16 * d_model more. */
+size_t ee_capture_bytes(const ee_model_config* cfg, int32_t rows);
+
+/* Test aid: record the values of every rounding site of the forward.  While
+ * `dev_buf` is non-NULL (device memory of `bytes` bytes, owned by the
+ * caller), every later block runs without graph replay and copies, for each
+ * layer in order, its x_attn (h * g of the attention-side norm, in the
+ * packed layout of GEMM inputs: fragments [R16 / 16][cols / KS][64 lanes]
+ * [16 B], KS = 32 for bf16 and 16 for fp32, where lane g * 16 + c of
+ * fragment (t, s) holds row 16 t + c, columns KS s + g KS / 4 .. + KS / 4), q after
+ * RoPE ([R][n_heads][head_dim]), the block's k after RoPE and v
+ * ([R][n_kv_heads][head_dim] each, in block row order), the attention output
+ * o (packed, qd columns), x_ffn (packed, d columns) and the SwiGLU product z
+ * (packed, ffn columns); after the last layer the LM head's input x_final
+ * (packed, d columns).  Every value is in the model dtype.  A block whose
+ * capture would exceed `bytes` fails with EE_EINVAL before it runs.
+ * dev_buf = NULL ends capturing.  These are the values a bf16 pipeline
+ * rounds (Eq. 3's forward; the rounding sites are a reading, since the paper
+ * states no precision), so a test can check every rounding decision of the
+ * GPU against the CPU reference. */
+int32_t ee_capture(ee_ctx* ctx, void* dev_buf, size_t bytes);
+
 /* Launch mode of later prefill/verify blocks.  on != 0 (the default): the
  * kernels of each block shape (row count, sequences, linear/tree/prefill, and
  * the attention splits of the longest context, ceil((n + T) / 256)) are
@@ -354,6 +381,14 @@ int32_t ee_time_gemm(ee_ctx* ctx, uint32_t cls, int32_t rows, int32_t reps, doub
 /* Message for the last failed call on ctx (or the last failed context-free
  * call when ctx is NULL).  Never NULL; the pointer stays valid until the next
  * call on the same context. */
+/* Measurement aid (no paper passage: infrastructure): microseconds per pass
+ * of a plain streaming read of `bytes` (a multiple of 16) of caller device
+ * memory at `dev_buf`, averaged over `reps` back-to-back passes on the
+ * context's stream after one untimed pass: the HBM read rate this GPU
+ * reaches in practice, which the verify step's rate is compared with.  The
+ * buffer is only read. */
+int32_t ee_time_stream_read(ee_ctx* ctx, const void* dev_buf, size_t bytes, int32_t reps, double* us_per_pass);
+
 const char* ee_last_error(const ee_ctx* ctx);
 
 #ifdef __cplusplus

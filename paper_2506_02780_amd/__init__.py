@@ -71,10 +71,13 @@ ee_match_reuse_c = _sig("ee_match_reuse", _i32, [_pi32, _i32, _pi32, _i32, _i32,
 ee_get_logits = _sig("ee_get_logits", _i32, [_vp, ctypes.POINTER(ctypes.c_float), _i32])
 ee_read_kv = _sig("ee_read_kv", _i32, [_vp, _i32, _i32, _vp, _vp])
 ee_load_kv = _sig("ee_load_kv", _i32, [_vp, _i32, _i32, _i32, _vp, _vp])
+ee_capture_bytes = _sig("ee_capture_bytes", _sz, [ctypes.POINTER(EEModelConfig), _i32])
+ee_capture = _sig("ee_capture", _i32, [_vp, _vp, _sz])
 ee_last_error = _sig("ee_last_error", ctypes.c_char_p, [_vp])
 ee_profile = _sig("ee_profile", _i32, [_vp, ctypes.c_uint32])
 ee_use_graphs = _sig("ee_use_graphs", _i32, [_vp, _i32])
 ee_time_gemm = _sig("ee_time_gemm", _i32, [_vp, ctypes.c_uint32, _i32, _i32, ctypes.POINTER(ctypes.c_double)])
+ee_time_stream_read = _sig("ee_time_stream_read", _i32, [_vp, _vp, _sz, _i32, ctypes.POINTER(ctypes.c_double)])
 ee_profile_read = _sig("ee_profile_read", _i32, [_vp, ctypes.POINTER(ctypes.c_double),
                                                  ctypes.POINTER(ctypes.c_int64), _i32])
 
@@ -335,6 +338,57 @@ class Engine:
             raise EEError(EE_EINVAL, "k and v must be [n_layers, n, n_kv_heads, head_dim]")
         _check(ee_load_kv(self.ctx, seq, k.shape[1], int(pending), k.ctypes.data, v.ctypes.data), self.ctx)
 
+    def capture(self, rows: int | None):
+        """Start (rows: the row count of the blocks to capture) or end (None)
+        recording every rounding site's values (ee_capture) into a device
+        buffer of this engine; ``captured()`` reads the last block's."""
+        if rows is None:     # the buffer stays readable until the next capture
+            _check(ee_capture(self.ctx, None, 0), self.ctx)
+            return
+        nb = ee_capture_bytes(ctypes.byref(self.cfg), int(rows))
+        if not nb:
+            raise EEError(EE_EINVAL, "invalid capture row count")
+        self._cap = torch.empty(nb, dtype=torch.uint8, device=self.device)
+        self._cap_rows = int(rows)
+        _check(ee_capture(self.ctx, self._cap.data_ptr(), nb), self.ctx)
+
+    def captured(self):
+        """{(site, layer): array} of the last captured block, in the model
+        dtype (bf16 bit patterns as uint16): x_attn, o, x_ffn, z [rows, cols]
+        and q [rows, n_heads, head_dim], k, v [rows, n_kv_heads, head_dim]
+        per layer; x_final [rows, d_model] at layer n_layers."""
+        s, R = self.shape, self._cap_rows
+        torch.cuda.synchronize(self.device)
+        raw = self._cap.cpu().numpy()
+        dt, esz, ks = (np.uint16, 2, 32) if s.dtype == "bf16" else (np.float32, 4, 16)
+        R16 = (R + 15) // 16 * 16
+        off = 0
+
+        def take(n):
+            nonlocal off
+            a = raw[off:off + n * esz].view(dt)
+            off += n * esz
+            return a
+
+        def packed(cols):
+            # fragments [R16/16][cols/KS][4 lane groups][16 lanes][KS/4 elements]
+            a = take(R16 * cols).reshape(R16 // 16, cols // ks, 4, 16, ks // 4)
+            return a.transpose(0, 3, 1, 2, 4).reshape(R16, cols)[:R]
+
+        out = {}
+        qd, kd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+        for l in range(s.n_layers):
+            out[("x_attn", l)] = packed(s.d_model)
+            out[("q", l)] = take(R * qd).reshape(R, s.n_heads, s.head_dim)
+            out[("k", l)] = take(R * kd).reshape(R, s.n_kv_heads, s.head_dim)
+            out[("v", l)] = take(R * kd).reshape(R, s.n_kv_heads, s.head_dim)
+            out[("o", l)] = packed(qd)
+            out[("x_ffn", l)] = packed(s.d_model)
+            out[("z", l)] = packed(s.ffn)
+        out[("x_final", s.n_layers)] = packed(s.d_model)
+        assert off == len(raw)
+        return out
+
     def use_graphs(self, on: bool):
         """Replay captured HIP graphs per block shape and attention split count
         (default) or launch eagerly."""
@@ -359,6 +413,14 @@ class Engine:
         layer in turn, back to back (ee_time_gemm)."""
         us = ctypes.c_double()
         _check(ee_time_gemm(self.ctx, PROF_CLASSES.index(cls), rows, reps, ctypes.byref(us)), self.ctx)
+        return us.value
+
+    def time_stream_read(self, buf: torch.Tensor, reps: int = 10) -> float:
+        """Microseconds per pass of a plain streaming read of the device
+        tensor ``buf`` (ee_time_stream_read)."""
+        us = ctypes.c_double()
+        nb = buf.numel() * buf.element_size() // 16 * 16
+        _check(ee_time_stream_read(self.ctx, buf.data_ptr(), nb, int(reps), ctypes.byref(us)), self.ctx)
         return us.value
 
     def close(self):

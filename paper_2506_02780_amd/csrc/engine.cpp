@@ -29,6 +29,7 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 thread_local std::string g_err = "no error";
 
+
 struct Seq {
   bool live = false;
   int len = 0;
@@ -90,6 +91,21 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   return true;
 }
 
+// Columns of the largest GEMM slice-partial array of a row: max over the
+// projections of K slices x output features.
+size_t partial_cols(const ee_model_config& g) {
+  const int dt = g.dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
+  const size_t d = g.d_model, qd = (size_t)g.n_heads * g.head_dim, F = g.ffn;
+  const size_t qkvN = qd + 2 * (size_t)g.n_kv_heads * g.head_dim;
+  size_t mx = 0;
+  mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * qkvN);
+  mx = std::max(mx, (size_t)ee::gemm_slices_for((int)qd, dt) * d);
+  mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * 2 * F);
+  mx = std::max(mx, (size_t)ee::gemm_slices_for((int)F, dt) * d);
+  mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * (size_t)g.vocab);
+  return mx;
+}
+
 Layout make_layout(const ee_model_config* c) {
   Layout L{};
   const size_t esz = c->dtype == EE_BF16 ? 2 : 4;
@@ -130,18 +146,8 @@ Layout make_layout(const ee_model_config* c) {
   L.zbuf = o; o += up(Tpad * F * esz);
   L.q = o; o += up(L.Rmax * H * hd * esz);
   L.part = o; o += up((size_t)L.max_splits * Hkv * L.Rmax * L.G * (hd + 2) * 4);
-  {
-    // split-K partials of the largest GEMM: [slices][Rmax][N]
-    const int dt = c->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
-    const size_t qkvN = (H + 2 * Hkv) * hd;
-    size_t mx = 0;
-    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * qkvN);
-    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)(H * hd), dt) * d);
-    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * 2 * F);
-    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)F, dt) * d);
-    mx = std::max(mx, (size_t)ee::gemm_slices_for((int)d, dt) * V);
-    L.gpart = o; o += up(mx * L.Rmax * 4);
-  }
+  // split-K partials of the largest GEMM: [slices][Rmax][N]
+  L.gpart = o; o += up(partial_cols(*c) * L.Rmax * 4);
   L.logits = o; o += up(L.Rmax * V * 4);
   L.amax = o; o += up(L.Rmax * ((V + 2047) / 2048) * 8 * 8);
   L.greedy = o; o += up(L.Rmax * 4);
@@ -203,6 +209,8 @@ struct ee_ctx {
   uint32_t* d_stage_src = nullptr;    // device-visible addresses of h_stage and h_result
   int* d_result_dst = nullptr;
   int last_T = 0;
+  unsigned char* cap = nullptr;       // ee_capture buffer (test aid) and its size
+  size_t cap_bytes = 0;
   std::string err = "no error";
   // profiling
   ee::Prof prof;
@@ -324,13 +332,13 @@ ee::StageCopy stage_ranges(const ee_ctx* c, const ee::Step& step) {
 
 // The kernels of one block, in launch order: staging in, forward, acceptance
 // (+ tree compaction), results out.
-hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof) {
+hipError_t launch_block(ee_ctx* c, const ee::Step& step, ee::Prof* prof, const ee::Work& w) {
   hipError_t e;
   if ((e = ee::run_stage_in(stage_ranges(c, step), c->st)) != hipSuccess) return e;
-  if ((e = ee::run_forward(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
-  if ((e = ee::run_accept(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
-  if (step.mode == 2 && (e = ee::run_compact(c->m, c->w, step, prof, c->st)) != hipSuccess) return e;
-  return ee::run_result_out(c->w, step.B, c->d_result_dst, c->st);
+  if ((e = ee::run_forward(c->m, w, step, prof, c->st)) != hipSuccess) return e;
+  if ((e = ee::run_accept(c->m, w, step, prof, c->st)) != hipSuccess) return e;
+  if (step.mode == 2 && (e = ee::run_compact(c->m, w, step, prof, c->st)) != hipSuccess) return e;
+  return ee::run_result_out(w, step.B, c->d_result_dst, c->st);
 }
 
 constexpr size_t MAX_GRAPHS = 512;   // captured block shapes kept at once
@@ -358,7 +366,7 @@ const ee_ctx::Captured* block_graph(ee_ctx* c, const ee::Step& step, ee::Prof* p
     return nullptr;
   }
   if (prof) prof->used = 0;
-  const hipError_t le = launch_block(c, step, prof);
+  const hipError_t le = launch_block(c, step, prof, c->w);
   const hipError_t ce = hipStreamEndCapture(c->st, &g);
   if (le != hipSuccess || ce != hipSuccess || !g || hipGraphInstantiate(&ge, g, nullptr, nullptr, 0) != hipSuccess) {
     if (g) (void)hipGraphDestroy(g);
@@ -410,18 +418,32 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
       slot[b * T + t] = s.pages[p / PAGE] * PAGE + p % PAGE;
     }
   }
+  if (c->cap) {
+    const ee_model_config& g = c->cfg;
+    const size_t need = ee::capture_bytes(g.n_layers, g.d_model, g.n_heads * g.head_dim, g.n_kv_heads * g.head_dim,
+                                          g.ffn, g.dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32, B * T);
+    if (need > c->cap_bytes) return fail(c, EE_EINVAL, "capture buffer too small for this block");
+  }
   int rc = order_after_user(c);
   if (rc) return rc;
-  const ee::Step step{T, B, mode, splits};
+  ee::Step step{T, B, mode, splits};
+  step.cap = c->cap;
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
-  // events recorded by graph nodes cannot be timed: profiled blocks run eagerly
-  const ee_ctx::Captured* cg = prof ? nullptr : block_graph(c, step, nullptr);
+  // events recorded by graph nodes cannot be timed, and captures are copies
+  // of a test aid: profiled or captured blocks run eagerly
+  const ee_ctx::Captured* cg = (prof || c->cap) ? nullptr : block_graph(c, step, nullptr);
   if (cg) {
     HIP_TRY(c, hipGraphLaunch(cg->exec, c->st));
     c->prof.used = cg->prof_pairs;
   } else {
     c->prof.used = 0;
-    HIP_TRY(c, launch_block(c, step, prof));
+    c->prof.overflow = false;
+    const hipError_t le = launch_block(c, step, prof, c->w);
+    if (le != hipSuccess) {
+      (void)hipStreamSynchronize(c->st);
+      if (c->prof.overflow) return fail(c, EE_EINVAL, "more timed launches in a block than profiling event pairs");
+      return hip_fail(c, le, "launch_block");
+    }
   }
   HIP_TRY(c, hipStreamSynchronize(c->st));
   for (int i = 0; prof && i < c->prof.used; ++i) {
@@ -970,6 +992,20 @@ int32_t ee_load_kv(ee_ctx* c, int32_t seq, int32_t n, int32_t pending, const voi
   return EE_OK;
 }
 
+size_t ee_capture_bytes(const ee_model_config* cfg, int32_t rows) {
+  if (!valid_cfg(cfg, nullptr) || rows < 1) return 0;
+  return ee::capture_bytes(cfg->n_layers, cfg->d_model, cfg->n_heads * cfg->head_dim, cfg->n_kv_heads * cfg->head_dim,
+                           cfg->ffn, cfg->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32, rows);
+}
+
+int32_t ee_capture(ee_ctx* c, void* dev_buf, size_t bytes) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (dev_buf && bytes == 0) return fail(c, EE_EINVAL, "a capture buffer needs a size");
+  c->cap = reinterpret_cast<unsigned char*>(dev_buf);
+  c->cap_bytes = dev_buf ? bytes : 0;
+  return EE_OK;
+}
+
 int32_t ee_use_graphs(ee_ctx* c, int32_t on) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
   c->graphs_on = on != 0;
@@ -980,8 +1016,8 @@ int32_t ee_profile(ee_ctx* c, uint32_t class_mask) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
   if (class_mask >> ee::PC_N) return fail(c, EE_EINVAL, "unknown profiling class");
   if (class_mask && c->events.empty()) {
-    // enough pairs for every launch of one block: 7 per layer plus a few
-    const int pairs = 8 * c->cfg.n_layers + 16;
+    // enough pairs for every timed launch of one block
+    const int pairs = ee::prof_pairs_per_block(c->cfg.n_layers);
     c->events.resize(2 * pairs);
     for (auto& e : c->events) {
       hipError_t r = hipEventCreate(&e);
@@ -1031,6 +1067,31 @@ int32_t ee_time_gemm(ee_ctx* c, uint32_t cls, int32_t rows, int32_t reps, double
   (void)hipEventDestroy(e1);
   if (e != hipSuccess) return hip_fail(c, e, "ee_time_gemm");
   *us_per_launch = (double)ms * 1e3 / ((double)reps * c->cfg.n_layers);
+  return EE_OK;
+}
+
+int32_t ee_time_stream_read(ee_ctx* c, const void* dev_buf, size_t bytes, int32_t reps, double* us_per_pass) {
+  if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
+  if (!dev_buf || !us_per_pass || reps < 1 || bytes < 16 || bytes % 16)
+    return fail(c, EE_EINVAL, "a buffer of a multiple of 16 bytes, reps >= 1 and an output are needed");
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  HIP_TRY(c, hipEventCreate(&e0));
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return fail(c, EE_EHIP, "hipEventCreate");
+  }
+  unsigned* sink = reinterpret_cast<unsigned*>(c->w.greedy);
+  hipError_t e = ee::run_stream_read(dev_buf, bytes, sink, c->st);   // warm-up pass
+  if (e == hipSuccess) e = hipEventRecord(e0, c->st);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = ee::run_stream_read(dev_buf, bytes, sink, c->st);
+  if (e == hipSuccess) e = hipEventRecord(e1, c->st);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return hip_fail(c, e, "ee_time_stream_read");
+  *us_per_pass = (double)ms * 1e3 / reps;
   return EE_OK;
 }
 

@@ -100,8 +100,15 @@ struct Prof {
   int* cls = nullptr;         // class of launch i
   int cap = 0;                // pairs available
   int used = 0;               // pairs recorded in the current block
+  bool overflow = false;      // a block had more timed launches than pairs
   bool on(int c) const { return (mask >> c) & 1u; }
 };
+
+// Timed launch scopes of one block, at most: per layer QKV, rotary + KV
+// append, attention, split merge, O, norm, gate/up, SwiGLU (unfused), down,
+// norm; then the first norm, LM head, logits, selection, acceptance and tree
+// compaction.
+inline int prof_pairs_per_block(int n_layers) { return 10 * n_layers + 6; }
 
 // Launch shape of one block.  Everything that changes from step to step
 // (committed lengths, split counts, tokens, positions, pages) is read by the
@@ -114,7 +121,12 @@ struct Step {
                 // 4 linear stochastic verify (one sequence)
   int splits;   // attention splits of the grid: the most any sequence of the
                 // block uses, ceil((n + T) / 256); 1 .. max_splits
+  unsigned char* cap = nullptr;   // test aid: copies of every rounding site's
+                                  // values (capture_bytes(m, T * B) bytes), or null
 };
+
+// Bytes of a rounding-site capture of R rows (layout in ee_capture's contract).
+size_t capture_bytes(int L, int d, int qdim, int kvdim, int F, int dt, int R);
 
 enum ProfClass {
   PC_NORM = 0, PC_QKV, PC_ATTN, PC_COMBINE, PC_OPROJ, PC_GATEUP, PC_DOWN, PC_LMHEAD, PC_ARGMAX,
@@ -139,6 +151,9 @@ hipError_t run_result_out(const Work& w, int B, int* host_result, hipStream_t st
 hipError_t run_forward(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_accept(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
 hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st);
+// One streaming read of `bytes` (a multiple of 16) at `buf`; `sink` is one
+// writable word (measurement aid).
+hipError_t run_stream_read(const void* buf, size_t bytes, unsigned* sink, hipStream_t st);
 // The GEMM of projection `which` (PC_QKV, PC_OPROJ, PC_GATEUP or PC_DOWN) for
 // every layer in turn, on R rows of the current activation buffers (timing).
 hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hipStream_t st);

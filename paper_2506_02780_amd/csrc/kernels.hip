@@ -661,7 +661,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
                                                          const float2* __restrict__ rope,
                                                          const int* __restrict__ rowslot,
                                                          void* __restrict__ q, void* __restrict__ kv_layer,
-                                                         const float* __restrict__ ssq, int d, float eps) {
+                                                         const float* __restrict__ ssq, int d, float eps,
+                                                         void* __restrict__ kv_cap) {
   const int t = blockIdx.y;
   const int half = hd >> 1;
   const int pairs = (H + 2 * Hkv) * half;
@@ -697,11 +698,21 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
       const size_t kb = (((size_t)page * 2 + 0) * Hkv + (head - H)) * 64 * hd + (size_t)sp * hd;
       store_elt<DT>(kv_layer, kb + i, y1);
       store_elt<DT>(kv_layer, kb + i + half, y2);
+      if (kv_cap) {   // test aid: the block's k rows, [T][Hkv][hd]
+        const size_t cb = ((size_t)t * Hkv + (head - H)) * hd;
+        store_elt<DT>(kv_cap, cb + i, y1);
+        store_elt<DT>(kv_cap, cb + i + half, y2);
+      }
     }
   } else {
     const size_t vb = (((size_t)page * 2 + 1) * Hkv + (head - H - Hkv)) * 64 * hd;
     store_elt<DT>(kv_layer, vb + (size_t)i * 64 + sp, x1);
     store_elt<DT>(kv_layer, vb + (size_t)(i + half) * 64 + sp, x2);
+    if (kv_cap) {     // test aid: the block's v rows after the k rows
+      const size_t cb = ((size_t)T * Hkv + (size_t)t * Hkv + (head - H - Hkv)) * hd;
+      store_elt<DT>(kv_cap, cb + i, x1);
+      store_elt<DT>(kv_cap, cb + i + half, x2);
+    }
   }
 }
 
@@ -1974,10 +1985,16 @@ __global__ __launch_bounds__(256) void compact_kernel(void* __restrict__ kv_pool
 
 // ------------------------------------------------------------- step driver --
 
-// Runs `launch` bracketed by profiling events when class `c` is selected.
+// Runs `launch` bracketed by profiling events when class `c` is selected.  A
+// block with more timed launches than event pairs fails (it is never timed
+// in part).
 template <typename F>
 static hipError_t timed(Prof* prof, int c, hipStream_t st, F&& launch) {
-  const bool on = prof && prof->on(c) && prof->used < prof->cap;
+  const bool on = prof && prof->on(c);
+  if (on && prof->used >= prof->cap) {
+    prof->overflow = true;
+    return hipErrorInvalidValue;
+  }
   hipError_t e;
   if (on && (e = hipEventRecord(prof->ev[2 * prof->used], st)) != hipSuccess) return e;
   if ((e = launch()) != hipSuccess) return e;
@@ -1988,7 +2005,51 @@ static hipError_t timed(Prof* prof, int c, hipStream_t st, F&& launch) {
   return hipSuccess;
 }
 
+// ------------------------------------------------------ streaming read --
+//
+// Measurement aid: the HBM read rate a plain streaming kernel reaches on this
+// part (the achievable bandwidth the verify step is also compared with).
+// Each thread keeps eight non-temporal 16-byte loads in flight; the loaded
+// words are folded into a value that is stored only in a case that does not
+// occur for the data measured (so the loads cannot be dropped).
+constexpr int STREAM_THREADS = 256, STREAM_UNROLL = 8;
+
+__global__ __launch_bounds__(STREAM_THREADS) void stream_read_kernel(const u32x4* __restrict__ p, size_t n16,
+                                                                     unsigned* __restrict__ sink) {
+  const size_t stride = (size_t)gridDim.x * STREAM_THREADS;
+  size_t i = (size_t)blockIdx.x * STREAM_THREADS + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + (STREAM_UNROLL - 1) * stride < n16; i += STREAM_UNROLL * stride) {
+    u32x4 v[STREAM_UNROLL];
+#pragma unroll
+    for (int j = 0; j < STREAM_UNROLL; ++j) v[j] = __builtin_nontemporal_load(p + i + j * stride);
+#pragma unroll
+    for (int j = 0; j < STREAM_UNROLL; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  }
+  for (; i < n16; i += stride) {
+    const u32x4 v = __builtin_nontemporal_load(p + i);
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
+hipError_t run_stream_read(const void* buf, size_t bytes, unsigned* sink, hipStream_t st) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipErrorInvalidValue;
+  const size_t want = (n16 + STREAM_THREADS * STREAM_UNROLL - 1) / (STREAM_THREADS * STREAM_UNROLL);
+  const int blocks = (int)std::min<size_t>(want, 256 * 8);   // 8 workgroups per CU
+  hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(STREAM_THREADS), 0, st,
+                     reinterpret_cast<const u32x4*>(buf), n16, sink);
+  return hipGetLastError();
+}
+
 int gemm_slices_for(int K, int dt) { return gemm_slices(K / ks_of(dt)); }
+
+size_t capture_bytes(int L, int d, int qdim, int kvdim, int F, int dt, int R) {
+  const size_t esz = esz_of(dt), R16 = (size_t)(R + 15) / 16 * 16;
+  const size_t layer = esz * (R16 * (2 * (size_t)d + qdim + F) + (size_t)R * (qdim + 2 * (size_t)kvdim));
+  return layer * L + esz * R16 * d;
+}
 
 template <int DT, int HD>
 static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* prof, hipStream_t st) {
@@ -2000,6 +2061,15 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   const size_t layer_elems = (size_t)m.max_pages * 2 * m.Hkv * 64 * m.hd;
   hipError_t e;
   auto last = [] { return hipGetLastError(); };
+  // test aid: per layer x_attn | q | k | v | o | x_ffn | z, then x_final
+  // (ee_capture); packed buffers of R16 rows
+  constexpr size_t ESZ = Geo<DT>::ESZ;
+  const size_t R16 = (size_t)(R + 15) / 16 * 16, kvdim = (size_t)m.Hkv * m.hd;
+  const size_t c_q = R16 * d * ESZ, c_k = c_q + (size_t)R * qdim * ESZ, c_o = c_k + 2 * (size_t)R * kvdim * ESZ;
+  const size_t c_xf = c_o + R16 * qdim * ESZ, c_z = c_xf + R16 * d * ESZ, c_layer = c_z + R16 * m.F * ESZ;
+  auto cap = [&](int l, size_t off, const void* src, size_t bytes) {
+    return hipMemcpyAsync(s.cap + (size_t)l * c_layer + off, src, bytes, hipMemcpyDeviceToDevice, st);
+  };
 
   if ((e = timed(prof, PC_NORM, st, [&] {
          hipLaunchKernelGGL((resid_kernel<DT, 0>), dim3((d + RES_COLS - 1) / RES_COLS, R), dim3(RES_THREADS), 0, st,
@@ -2007,6 +2077,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          return last();
        })) != hipSuccess)
     return e;
+  if (s.cap && (e = cap(0, 0, w.xbuf, R16 * d * ESZ)) != hipSuccess) return e;
 
   const int G = m.H / m.Hkv, ncols = T * G;   // query columns per sequence
   // the grid covers the splits of the block's longest context; a shorter
@@ -2024,10 +2095,12 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
            hipLaunchKernelGGL((qkv_finish_kernel<DT>), dim3((pairs + 255) / 256, R), dim3(256), 0, st, w.part,
-                              sk_d, R, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.slot, w.q, kvl, w.ssq, d, m.eps);
+                              sk_d, R, qkvN, m.H, m.Hkv, m.hd, w.pos, m.rope, w.slot, w.q, kvl, w.ssq, d, m.eps,
+                              s.cap ? (void*)(s.cap + (size_t)l * c_layer + c_k) : nullptr);
            return last();
          })) != hipSuccess)
       return e;
+    if (s.cap && (e = cap(l, c_q, w.q, (size_t)R * qdim * ESZ)) != hipSuccess) return e;
     // attention
     AttnArgs aa{};
     aa.q = w.q; aa.kv_layer = kvl; aa.ptable = w.ptable; aa.pos = w.pos; aa.path = w.path;
@@ -2086,6 +2159,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            return last();
          })) != hipSuccess)
       return e;
+    if (s.cap && (e = cap(l, c_o, w.xbuf, R16 * qdim * ESZ)) != hipSuccess) return e;
     // O projection; residual add + FFN norm
     if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, R, w.part, st); })) != hipSuccess)
       return e;
@@ -2095,6 +2169,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            return last();
          })) != hipSuccess)
       return e;
+    if (s.cap && (e = cap(l, c_xf, w.xbuf, R16 * d * ESZ)) != hipSuccess) return e;
     // gate/up projection and SwiGLU: fused for d / KS <= FK_MAX_S, else
     // split-K partials and a SwiGLU launch
     if (fused_swiglu(d, DT)) {
@@ -2113,6 +2188,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            })) != hipSuccess)
         return e;
     }
+    if (s.cap && (e = cap(l, c_z, w.zbuf, R16 * m.F * ESZ)) != hipSuccess) return e;
     // down projection; residual add + the next norm (layer l+1 attention side, or final)
     if ((e = timed(prof, PC_DOWN, st, [&] { return gemm<DT>(lp.wd, w.zbuf, d, m.F, R, w.part, st); })) != hipSuccess)
       return e;
@@ -2123,6 +2199,8 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            return last();
          })) != hipSuccess)
       return e;
+    // x_attn of the next layer, or (after the last layer) x_final
+    if (s.cap && (e = cap(l + 1, 0, w.xbuf, R16 * d * ESZ)) != hipSuccess) return e;
   }
   // LM head, logits + chunk maxima, argmax
   if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); })) != hipSuccess)

@@ -89,7 +89,7 @@ def test_sample_verification_matches_oracle(ee, draft_kind, residual, temp):
         eng.rollback(0, n0, p0)
         rl = ref.score(draft)
         err = float(np.abs(gl - rl).max())
-        assert err <= 1e-3
+        assert err <= 3 * 1e-4           # the stated fp32 tolerance, scaled with the logits (gain x3)
         e64, u64 = eps.astype(np.float64), u.astype(np.float64)
         ra, rn = accept_sample(draft, rl, e64, u64, q, temp, residual)
         if _unique(list(draft), rl, e64, u64, q, temp, residual, err):

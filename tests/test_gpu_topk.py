@@ -14,6 +14,7 @@ span low and high entropies.
 import numpy as np
 import pytest
 
+from helpers import adopt_outcome
 from oracle import OracleSession, accept_topk, entropy_threshold, topk_tokens
 from workloads import gen_weights, get_shape, planted_draft, zipf_tokens
 
@@ -34,12 +35,12 @@ def _model(cfg):
         shape = get_shape("tiny", vocab=32000)
         w = gen_weights(shape, seed=21, std=0.1)
         w.final_gain = (w.final_gain * 4.0).astype(np.float32)
-        return shape, w, 2e-3
+        return shape, w, 4 * 1e-4          # the stated fp32 tolerance, scaled with the logits
     shape = get_shape("tiny", n_layers=2, d_model=512, n_heads=4, n_kv_heads=2, head_dim=128, ffn=1024,
                       vocab=5024, dtype="bf16")   # 3 chunks, the last one partial
     w = gen_weights(shape, seed=22, std=0.02)
     w.final_gain = (w.final_gain * 8.0).astype(np.float32)   # a power of two: bf16 rounding unchanged
-    return shape, w, 0.2
+    return shape, w, 8 * 2e-2          # the stated bf16 tolerance, scaled with the logits
 
 
 def _ranked_draft(ref, K, g):
@@ -65,7 +66,7 @@ def _row_unique(row, gpu_row, k, dynamic, err):
 
 def _compare(gpu_res, gpu_logits, ref_logits, draft, k, dynamic, tol, seen):
     """Compare one step; returns False when a non-unique decision differed
-    (the two sessions then diverge and the comparison stops)."""
+    (the oracle then follows the GPU's outcome, reading G12)."""
     a, nxt, thr = gpu_res
     K = len(draft)
     err = float(np.abs(gpu_logits - ref_logits).max())
@@ -94,7 +95,7 @@ def test_topk_session_matches_oracle(ee, cfg, k, dynamic):
     eng = ee.Engine(shape, w, max_ctx=256, k_max=12)
     assert eng.prefill(0, prompt) == ref.prefill(prompt)
     g = np.random.default_rng(k + 10 * dynamic)
-    seen, pinned, accepted_beyond_greedy = [], 0, 0
+    seen, compared, unpinned, accepted_beyond_greedy = [], 0, 0, 0
     # bf16 logits are ~0.04 apart from the oracle's, so few rows have a unique
     # dynamic threshold (k H must lie 3 k err from an integer): more steps
     steps = 8 if cfg == "f32" else 24
@@ -102,22 +103,29 @@ def test_topk_session_matches_oracle(ee, cfg, k, dynamic):
         K = int(g.integers(0, 13)) if step else 0
         draft = _ranked_draft(ref, K, g)
         res = eng.verify_topk([0], [draft], k, dynamic)[0]
+        saved = (ref.cache, ref.pending)
         ra, rn, _ = ref.verify_topk(draft, k, dynamic)
         if not _compare(res, eng.logits(), ref.last_logits, draft, k, dynamic, tol, seen):
-            break
-        pinned += 1
+            # a near tie (rank or threshold) decided the GPU's way: the oracle
+            # commits the GPU's outcome and the session goes on
+            adopt_outcome(ref, saved, draft, res[0], res[1])
+            unpinned += 1
+            ra = res[0]
+        compared += 1
         assert eng.seq_state(0) == (ref.n, ref.pending)
         accepted_beyond_greedy += sum(int(draft[i]) != int(np.argmax(ref.last_logits[i])) for i in range(ra))
     eng.close()
-    print(f"pinned {pinned} steps, {len(seen)} thresholds compared, values {sorted(set(seen))}")
+    print(f"{compared} steps compared, {unpinned} near ties followed, {len(seen)} thresholds compared, "
+          f"values {sorted(set(seen))}")
+    assert compared == steps
     if cfg == "f32":
-        assert pinned == steps
+        assert unpinned == 0
         assert len(seen) >= 30
         assert accepted_beyond_greedy >= 3
         if dynamic:
             assert len(set(seen)) >= 2
     else:
-        assert pinned >= 1 and len(seen) >= 5
+        assert unpinned <= steps // 3 and len(seen) >= 5
 
 
 def _bf16_engine(ee, prompts, k_max=16):
