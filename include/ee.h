@@ -140,6 +140,30 @@ int32_t ee_verify(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t
                   const int32_t* parent, int32_t* accept_len, int32_t* next_token,
                   int32_t* accepted_nodes);
 
+/* ee_verify for callers that cannot allocate memory (serving loops and
+ * harnesses that forbid device or host allocation during a step): the same
+ * arguments, checks, kernels and results (bit for bit) as ee_verify, but the
+ * step's scratch (the attention split states and the GEMM K-slice partials)
+ * lives in a static device array of the library, 16 MiB per GPU (held by
+ * each GPU the library runs on until the process ends), instead of the
+ * context's workspace, and the block runs without graph capture or replay, so
+ * the call allocates nothing (no hipMalloc, hipFree, graph instantiation or
+ * other allocating routine).  The array's device address is looked up once
+ * per GPU by ee_create, and the context's GPU must be the current device at
+ * the call (else EE_EINVAL).  A block whose scratch exceeds 16 MiB fails with
+ * EE_ECAPACITY before anything runs; it needs
+ *   up(ceil((len + K + 1) / 256) * n_kv_heads * (K + 1) * (n_heads / n_kv_heads) * (head_dim + 2) * 4)
+ *   + up(S * (K + 1) * 4)
+ * bytes, up() rounding to 256, S = the largest K-slice count times output
+ * width over the projections and the LM head (7B-class bf16, K = 32 over a
+ * 2048-position context: 13.4 MB).  Every call on a GPU shares that GPU's
+ * array and leaves its contents behind (every value a call reads there is
+ * written earlier in the same call); calls on one GPU must not overlap, or
+ * they race on it. */
+int32_t ee_verify_noalloc(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, int32_t K,
+                          const int32_t* parent, int32_t* accept_len, int32_t* next_token,
+                          int32_t* accepted_nodes);
+
 /* ee_verify for n_seq distinct sequences in one block (n_seq <= max_seqs),
  * all with the same draft length K: drafts[b*K .. b*K + K-1] is the draft of
  * sequence seqs[b]; parents (NULL: every draft is a linear chain) holds

@@ -59,6 +59,7 @@ ee_create = _sig("ee_create", _i32, [ctypes.POINTER(EEModelConfig), ctypes.POINT
 ee_destroy = _sig("ee_destroy", _i32, [_vp])
 ee_prefill = _sig("ee_prefill", _i32, [_vp, _i32, _pi32, _i32, _pi32])
 ee_verify = _sig("ee_verify", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
+ee_verify_noalloc = _sig("ee_verify_noalloc", _i32, [_vp, _i32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_batch = _sig("ee_verify_batch", _i32, [_vp, _i32, _pi32, _pi32, _i32, _pi32, _pi32, _pi32, _pi32])
 ee_verify_topk = _sig("ee_verify_topk", _i32, [_vp, _i32, _pi32, _pi32, _i32, _i32, _i32, _pi32, _pi32, _pi32])
 _pf32 = ctypes.POINTER(ctypes.c_float)
@@ -229,6 +230,24 @@ class Engine:
         _check(ee_verify(self.ctx, seq, dp, k, None, ctypes.byref(a), ctypes.byref(nxt), None), self.ctx)
         self._last_rows = k + 1
         return a.value, nxt.value, None
+
+    def verify_noalloc(self, seq: int, draft, parent=None):
+        """ee_verify_noalloc: ee_verify with the step's scratch in the
+        library's static device array (no allocation, no graph).  Returns
+        (accept_len, next_token, accepted_nodes or None)."""
+        d, dp = _i32arr(draft)
+        k = len(d)
+        a, nxt = ctypes.c_int32(), ctypes.c_int32()
+        pp, nodes = None, None
+        if parent is not None:
+            p, pp = _i32arr(parent)
+            if len(p) != k:
+                raise EEError(EE_EINVAL, "parent must have one entry per draft node")
+            nodes = np.zeros(max(k, 1), dtype=np.int32)
+        _check(ee_verify_noalloc(self.ctx, seq, dp, k, pp, ctypes.byref(a), ctypes.byref(nxt),
+                                 nodes.ctypes.data_as(_pi32) if nodes is not None else None), self.ctx)
+        self._last_rows = k + 1
+        return a.value, nxt.value, (nodes[:a.value].copy() if nodes is not None else None)
 
     def verify_batch(self, seqs, drafts, parents=None):
         """One block for several sequences; drafts (and parents) are equal-length

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <map>
+#include <mutex>
 #include <tuple>
 #include <new>
 #include <string>
@@ -27,8 +28,38 @@ constexpr size_t ALIGN = 256;
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
+// Scratch of ee_verify_noalloc: the step's attention split states and GEMM
+// slice partials, in a static device array (one per GPU the library runs on,
+// held until the process ends) instead of the caller's workspace.
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(16) << 20;
+constexpr int MAX_DEVICES = 64;
+
 thread_local std::string g_err = "no error";
 
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_addr[MAX_DEVICES] = {};   // device address of `scratch` on each GPU
+
+// The device address of this GPU's `scratch` (the array's name is only a
+// host-side stand-in), looked up once per device with that device current.
+hipError_t scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
 
 struct Seq {
   bool live = false;
@@ -209,6 +240,8 @@ struct ee_ctx {
   uint32_t* d_stage_src = nullptr;    // device-visible addresses of h_stage and h_result
   int* d_result_dst = nullptr;
   int last_T = 0;
+  int dev = -1;                       // GPU of the context (current at ee_create)
+  unsigned char* scratch = nullptr;   // that GPU's static scratch array (ee_verify_noalloc)
   unsigned char* cap = nullptr;       // ee_capture buffer (test aid) and its size
   size_t cap_bytes = 0;
   std::string err = "no error";
@@ -399,7 +432,10 @@ int order_after_user(ee_ctx* c) {
 // mirror and write the results to h_result, record b at h_result + b *
 // (2 + k_max)) and wait for it.  Mode 3 uses the top-k size and dynamic flag
 // given for every sequence.
-int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0, int dynamic = 0) {
+// `scratch_work`: buffers of the block when they are not the context's own
+// (ee_verify_noalloc); such a block runs without graph replay.
+int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0, int dynamic = 0,
+              const ee::Work* scratch_work = nullptr) {
   const Layout& L = c->lay;
   int* ptab = reinterpret_cast<int*>(c->h_stage + L.s_ptable);
   int* info = reinterpret_cast<int*>(c->h_stage + L.s_info);
@@ -431,14 +467,14 @@ int run_block(ee_ctx* c, Seq* const* seqs, int B, int T, int mode, int top_k = 0
   ee::Prof* prof = c->prof.mask ? &c->prof : nullptr;
   // events recorded by graph nodes cannot be timed, and captures are copies
   // of a test aid: profiled or captured blocks run eagerly
-  const ee_ctx::Captured* cg = (prof || c->cap) ? nullptr : block_graph(c, step, nullptr);
+  const ee_ctx::Captured* cg = (prof || c->cap || scratch_work) ? nullptr : block_graph(c, step, nullptr);
   if (cg) {
     HIP_TRY(c, hipGraphLaunch(cg->exec, c->st));
     c->prof.used = cg->prof_pairs;
   } else {
     c->prof.used = 0;
     c->prof.overflow = false;
-    const hipError_t le = launch_block(c, step, prof, c->w);
+    const hipError_t le = launch_block(c, step, prof, scratch_work ? *scratch_work : c->w);
     if (le != hipSuccess) {
       (void)hipStreamSynchronize(c->st);
       if (c->prof.overflow) return fail(c, EE_EINVAL, "more timed launches in a block than profiling event pairs");
@@ -661,6 +697,20 @@ int32_t ee_create(const ee_model_config* cfg, const ee_weights* wts, void* packe
     return cleanup(EE_EHIP);
   }
 
+  // this GPU's static scratch array (ee_verify_noalloc), looked up once per device
+  if ((e = hipGetDevice(&c->dev)) != hipSuccess) {
+    hip_fail(c, e, "hipGetDevice");
+    return cleanup(EE_EHIP);
+  }
+  {
+    void* sp = nullptr;
+    if ((e = scratch_address(c->dev, &sp)) != hipSuccess) {
+      hip_fail(c, e, "hipGetSymbolAddress(scratch)");
+      return cleanup(EE_EHIP);
+    }
+    c->scratch = reinterpret_cast<unsigned char*>(sp);
+  }
+
   // pack weights
   auto run = [&](hipError_t err, const char* where) {
     if (err != hipSuccess) { hip_fail(c, err, where); return false; }
@@ -798,6 +848,52 @@ int32_t ee_verify(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const
   stage_draft(c, 0, T, s, draft, parent, depth);
   Seq* one = &s;
   rc = run_block(c, &one, 1, T, parent ? 2 : 1);
+  if (rc) {
+    unreserve(c, s, added);
+    return rc;
+  }
+  const int a = c->h_result[0];
+  s.len += 1 + a;
+  s.pending = c->h_result[1];
+  *accept_len = a;
+  *next_token = s.pending;
+  if (accepted_nodes)
+    for (int i = 0; i < a; ++i) accepted_nodes[i] = c->h_result[2 + i] - 1;
+  return EE_OK;
+}
+
+int32_t ee_verify_noalloc(ee_ctx* c, int32_t seq, const int32_t* draft, int32_t K, const int32_t* parent,
+                          int32_t* accept_len, int32_t* next_token, int32_t* accepted_nodes) {
+  int rc = check_seq(c, seq);
+  if (rc) return rc;
+  if (!accept_len || !next_token) return fail(c, EE_EINVAL, "accept_len and next_token must be non-NULL");
+  Seq& s = c->seqs[seq];
+  if (!s.live || s.pending < 0) return fail(c, EE_ESTATE, "verify before prefill");
+  if (K < 0 || K > c->cfg.k_max) return fail(c, EE_EINVAL, "K outside [0, k_max]");
+  if (parent && K > MAX_TREE) return fail(c, EE_EINVAL, "draft trees have at most 64 nodes");
+  int depth[MAX_TREE + 1];
+  if ((rc = check_draft(c, draft, K, parent, depth))) return rc;
+  const int T = K + 1;
+  if (s.len + T > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "block would exceed max_ctx");
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != c->dev)
+    return fail(c, EE_EINVAL, "the context's GPU must be the current device");
+  // scratch of this block: attention split states, then GEMM slice partials
+  const ee_model_config& g = c->cfg;
+  const size_t splits = (size_t)(s.len + T + SPLIT - 1) / SPLIT;
+  const size_t attn = up(splits * g.n_kv_heads * (size_t)T * (g.n_heads / g.n_kv_heads) * (g.head_dim + 2) * 4);
+  const size_t part = up(partial_cols(g) * (size_t)T * 4);
+  if (attn + part > NOALLOC_SCRATCH_BYTES)
+    return fail(c, EE_ECAPACITY, "this block needs " + std::to_string(attn + part) +
+                                     " bytes of scratch, more than the 16 MiB static buffer of ee_verify_noalloc");
+  int added;
+  if (!reserve_pages(c, s, s.len + T, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");
+  stage_draft(c, 0, T, s, draft, parent, depth);
+  ee::Work w = c->w;
+  w.attn_part = reinterpret_cast<float*>(c->scratch);
+  w.part = reinterpret_cast<float*>(c->scratch + attn);
+  Seq* one = &s;
+  rc = run_block(c, &one, 1, T, parent ? 2 : 1, 0, 0, &w);
   if (rc) {
     unreserve(c, s, added);
     return rc;
