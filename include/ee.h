@@ -24,6 +24,13 @@
  *  - Return codes: EE_OK (0) or a negative EE_E* value; ee_last_error gives a
  *    message for the last failure on a context.
  *  - A context is not thread-safe; calls on one context must not overlap.
+ *
+ * Calls with no passage of the paper behind them are infrastructure: sizing
+ * (ee_*_bytes), ee_create / ee_destroy, ee_seq_state, ee_use_graphs,
+ * ee_last_error, the test aids (ee_get_logits, ee_read_kv, ee_load_kv,
+ * ee_capture) and the measurement aids (ee_profile, ee_profile_read,
+ * ee_time_gemm, ee_time_stream_read).  Every other call names the passage
+ * it implements.
  */
 #ifndef EE_H
 #define EE_H
@@ -88,7 +95,7 @@ size_t ee_packed_weight_bytes(const ee_model_config* cfg);
 size_t ee_kv_pool_bytes(const ee_model_config* cfg);
 size_t ee_workspace_bytes(const ee_model_config* cfg);
 
-/* Build a context.  Packs every weight into `packed` (the library's
+/* Build a context (infrastructure).  Packs every weight into `packed` (the library's
  * MFMA-fragment layout) and zeroes `kv_pool`, on `hip_stream` (a hipStream_t;
  * NULL = the default stream), then synchronizes that stream.  Every later
  * call runs its GPU work on a stream of the context's own, ordered after the
@@ -101,7 +108,9 @@ int32_t ee_destroy(ee_ctx* ctx);
 /* Run the prompt tokens[0..n-1] of sequence `seq` (which must be empty) in
  * blocks of at most k_max+1 rows, commit all n positions to the KV cache and
  * return the greedy token of the last row in *next_token: the first emitted
- * token, now "pending" (emitted, not yet run through the model).  n >= 1.   */
+ * token of plain greedy decoding (Eq. 1, the argmax of the target's
+ * distribution given the prompt), now "pending" (emitted, not yet run through
+ * the model).  n >= 1.   */
 int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
                    int32_t* next_token);
 
@@ -221,7 +230,10 @@ int32_t ee_verify_sample(ee_ctx* ctx, int32_t seq, const int32_t* draft_tokens, 
 
 /* Truncate sequence `seq` to its first new_len committed positions
  * (new_len <= len), release pages wholly beyond them and make pending_token
- * pending.  new_len == 0 with pending_token == -1 empties the sequence (it
+ * pending: the rewind of the cache to an earlier prefix (Sec. "Reuse": after
+ * a rejection only the accepted prefix stays, the remaining drafts being
+ * candidates for later steps; ee_verify already commits exactly that, and this
+ * call rewinds explicitly, e.g. to re-verify from an earlier position).  new_len == 0 with pending_token == -1 empties the sequence (it
  * may then be prefilled again).  EE_ESTATE if new_len > len. */
 int32_t ee_kv_rollback(ee_ctx* ctx, int32_t seq, int32_t new_len, int32_t pending_token);
 

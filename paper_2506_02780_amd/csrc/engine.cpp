@@ -110,6 +110,11 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
     if (layer >= (size_t(1) << 31)) return bad("one layer of the KV pool must stay below 2 GiB");
   }
   {
+    // the packed LM head and embedding are addressed with 32-bit buffer offsets
+    const size_t head = (size_t)c->vocab * c->d_model * (c->dtype == EE_BF16 ? 2 : 4);
+    if (head >= (size_t(1) << 31)) return bad("vocab * d_model of the LM head must stay below 2 GiB");
+  }
+  {
     // GEMM slice partials of one block are written through 32-bit buffer offsets
     const int dt = c->dtype == EE_BF16 ? ee::DT_BF16 : ee::DT_F32;
     const size_t rows = (size_t)(c->k_max + 1) * c->max_seqs;

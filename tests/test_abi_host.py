@@ -47,6 +47,13 @@ def test_config_sizes_and_validation():
     rc = ee.ee_create(ctypes.byref(bad), ctypes.byref(w), 1, 1, 1, None, ctypes.byref(ctx))
     assert rc == ee.EE_EINVAL and b"head_dim" in ee.ee_last_error(None)
     assert ee.ee_destroy(None) == ee.EE_EINVAL
+    # an LM head of 2 GiB or more (vocab 152064 x d 8192 in bf16) is refused:
+    # it is addressed with 32-bit offsets
+    huge = ee.make_config(get_shape("7b", d_model=8192, vocab=152064), max_ctx=128)
+    assert ee.ee_workspace_bytes(ctypes.byref(huge)) == 0
+    rc = ee.ee_create(ctypes.byref(huge), ctypes.byref(w), 1, 1, 1, None, ctypes.byref(ctx))
+    assert rc == ee.EE_EINVAL and b"LM head" in ee.ee_last_error(None)
+    assert ee.ee_capture_bytes(ctypes.byref(cfg), 33) > 0 and ee.ee_capture_bytes(ctypes.byref(cfg), 0) == 0
 
 
 def test_null_context_calls_fail_cleanly():
@@ -58,6 +65,9 @@ def test_null_context_calls_fail_cleanly():
     assert ee.ee_verify_topk(None, 1, None, None, 0, 3, 1, None, None, None) == ee.EE_EINVAL
     assert ee.ee_extend(None, 0, None, 0, ctypes.byref(a)) == ee.EE_EINVAL
     assert ee.ee_time_gemm(None, 5, 1, 1, None) == ee.EE_EINVAL
+    assert ee.ee_time_stream_read(None, None, 16, 1, None) == ee.EE_EINVAL
+    assert ee.ee_capture(None, None, 0) == ee.EE_EINVAL
+    assert ee.ee_verify_noalloc(None, 0, None, 0, None, ctypes.byref(a), ctypes.byref(a), None) == ee.EE_EINVAL
     assert ee.ee_edit_begin(None, 0, None, 0, None) == ee.EE_EINVAL
 
 
