@@ -4,18 +4,27 @@
 Workload (synthetic stand-in for the paper's code-editing benchmarks): a
 7B-class Llama-style decoder with random bf16 weights, a 2048-token Zipf
 prompt, and an "original code" c made from the model's own 512-token greedy
-continuation G with 5% of its positions replaced in 3-8-token spans.  Every
-timed step is one Reuse-phase step: the matcher picks where the generated
-output continues in c (a suffix match of at least 3 tokens, else the
-position right after the last verified draft), K = 32 tokens of c from there are verified in one
-forward, and the accepted prefix plus the target's next token are emitted.
-When G has been re-created in full the sequence is rolled back to the prompt.
-The emitted stream is checked to equal G (greedy verification is lossless).
+continuation G with 5% of its positions replaced in 3-8-token spans.  A
+benchmark step is one edit task: the whole Reuse session that re-creates G
+from c after the prompt.  Each verify call of it is one pass of the hot path:
+the matcher picks where the generated output continues in c (a suffix match
+of at least 3 tokens, else the position right after the last verified
+draft), K = 32 tokens of c from there are verified in one forward, and the
+accepted prefix plus the target's next token are emitted.  Every session is
+checked to re-create G exactly (greedy verification is lossless), and every
+session makes the same verify calls, so tokens/s does not depend on how many
+steps are timed.
 
-Printed: one JSON line.  value = emitted tokens per second of the Reuse
-session (the paper's Tokens/s); also the verify-step latency at exactly 2048
-committed positions, the whole-step HBM roofline fraction, the dominant
-kernel's live roofline and the CPU oracle's rate on a bounded sample.
+Printed: one JSON line.  value = emitted tokens per second over the timed
+sessions (the paper's Tokens/s); also the verify-step latency at exactly 2048
+committed positions (p50/p90 of 200 calls after 20 warm-up calls), the
+whole-step HBM fraction of the 8 TB/s peak and of the streaming-read rate
+measured on this GPU, each projection's rate, the dominant kernel's live
+roofline and the CPU oracle's rate.
+
+Other modes: --profile-only runs only fixed-context K = 32 verify steps and
+the projection timing sequences (for rocprofv3); --rocprof-summary DIR
+reduces rocprofv3's CSV output to the tables kept with the profiles.
 """
 
 from __future__ import annotations
@@ -66,6 +75,19 @@ def gateup_bytes(s, t: int) -> int:
     return esz * (2 * s.ffn * s.d_model + t * s.d_model + t * s.ffn)
 
 
+def projection_model(s, cls: str, t: int):
+    """(N, K, algorithmic bytes, flops) of one projection launch on t rows:
+    the [N, K] weights once, the t input rows, and the t output rows (fp32
+    results; the fused gate/up writes its t x F SwiGLU products in the model
+    dtype instead)."""
+    esz = 2 if s.dtype == "bf16" else 4
+    d, qd, kd, f = s.d_model, s.q_dim, s.kv_dim, s.ffn
+    n, k = {"qkv": (qd + 2 * kd, d), "oproj": (d, qd), "gateup": (2 * f, d), "down": (d, f),
+            "lmhead": (s.vocab, d)}[cls]
+    out = t * f * esz if cls == "gateup" else t * n * 4
+    return n, k, esz * (n * k + t * k) + out, 2 * t * n * k
+
+
 def _gemm_source_digest(path):
     """sha256 of the fused gate/up + SwiGLU section of the kernel source (from
     its section banner to the next one): the code the counter figures were
@@ -98,48 +120,59 @@ def measured_traffic():
     return int(fields["gateup_traffic_bytes_per_launch"])
 
 
-def cpu_baseline(shape, weights, k: int, ctx: int, layers: int, emitted_per_step: float):
-    """Time the oracle on a bounded sample of one verify step and scale it."""
+def cpu_info() -> dict:
+    """CPU model and core count of this host."""
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count()}
+
+
+def cpu_baseline(shape, weights, k: int, ctx: int, steps: int, emitted_per_verify: float):
+    """The oracle (float64 NumPy, as it stands) timed on this host: `steps`
+    whole K = k verify steps through all layers over a `ctx`-position
+    committed cache, and one K = 0 step.  The committed cache is a seeded
+    random bf16 one (the oracle's own 2048-token prefill would take minutes);
+    the per-layer widening of the bf16 weights to float64, which the oracle
+    does inside its forward, is part of the time."""
     from threadpoolctl import threadpool_info
 
-    from oracle import forward_block, tree_structure  # noqa: F401
-    from oracle.model import chain_structure
+    from oracle import OracleSession
     from oracle.numerics import to_f64
     from workloads import random_kv_context, zipf_tokens
 
-    class Sub:
-        def __init__(self, w, nl):
-            self.embed, self.lm_head, self.final_gain = w.embed, w.lm_head, w.final_gain
-            self._w, self._nl = w, nl
-
-        def layer(self, l):
-            return self._w.layer(l)
-
-    tokens = zipf_tokens(shape.vocab, k + 1, seed=3)
-    depth, vis = chain_structure(k + 1)
-    kv = random_kv_context(layers, ctx, shape.n_kv_heads, shape.head_dim, seed=5, dtype=shape.dtype)
+    kv = random_kv_context(shape.n_layers, ctx, shape.n_kv_heads, shape.head_dim, seed=5, dtype=shape.dtype)
     cache = [(to_f64(a, shape.dtype), to_f64(b, shape.dtype)) for a, b in kv]
+    del kv
+    pending = int(zipf_tokens(shape.vocab, 1, seed=3)[0])
 
-    def run(nl):
-        sub = shape.with_(n_layers=nl)
+    def run(draft):
+        ref = OracleSession(shape, weights)
+        ref.set_cache(cache, pending)
         t0 = time.perf_counter()
-        forward_block(sub, Sub(weights, nl), cache[:nl], tokens, depth, vis)
+        ref.verify(draft)
         return time.perf_counter() - t0
 
-    t_head = min(run(0) for _ in range(2))
-    t_layers = min(run(layers) for _ in range(2))
-    per_layer = max(t_layers - t_head, 0.0) / layers
-    est = t_head + per_layer * shape.n_layers
+    times = [run(zipf_tokens(shape.vocab, k, seed=10 + i)) for i in range(steps)]
+    t_ar = run(np.zeros(0, dtype=np.int32))
+    per = float(np.mean(times))
     threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    info = cpu_info()
     return {
-        "value": round(emitted_per_step / est, 3), "unit": "tokens/s", "cores": int(threads),
+        "value": round(emitted_per_verify / per, 4), "unit": "tokens/s", "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"one K={k} verify block over a {ctx}-position committed KV cache (random bf16 "
-                   f"values) through {layers} of the {shape.n_layers} layers plus final norm and LM "
-                   f"head, fp64 NumPy; step time = head part + {shape.n_layers}/{layers} x layer part "
-                   f"= {est:.2f} s; tokens/s uses the GPU session's {emitted_per_step:.2f} emitted "
-                   f"tokens per step"),
-        "step_seconds": round(est, 3),
+        "sample": (f"{steps} whole K={k} verify steps ({shape.n_layers} layers, LM head and acceptance) "
+                   f"over a {ctx}-position committed cache of seeded random bf16 values, float64 NumPy, "
+                   f"{per:.2f} s per step; tokens/s uses the GPU session's {emitted_per_verify:.2f} emitted "
+                   f"tokens per verify call; plus one K=0 step (one plain greedy token) in {t_ar:.2f} s"),
+        "verify_step_seconds": [round(t, 3) for t in times],
+        "k0_step_seconds": round(t_ar, 3),
+        "cpu_model": info["model"], "logical_cpus": info["logical_cpus"], "blas_threads": int(threads),
     }
 
 
@@ -274,22 +307,184 @@ def attention_flops(s, t: int, n: int) -> int:
     return s.n_layers * 2 * 2 * s.n_heads * s.head_dim * t * (n + (t + 1) // 2)
 
 
+def projection_rates(eng, shape, t: int) -> dict:
+    """Each projection's GEMM (and the LM head's) on t rows, launched for
+    every layer in turn, 3 times, back to back between two HIP events
+    (ee_time_gemm): microseconds per launch, algorithmic HBM rate and
+    matrix-core rate (t rows, no padding) against the peaks."""
+    out = {}
+    for cls in ("qkv", "oproj", "gateup", "down", "lmhead"):
+        us = eng.time_gemm(cls, t, reps=3)
+        n, k, nbytes, flops = projection_model(shape, cls, t)
+        out[cls] = {"n": n, "k": k, "us_per_launch": round(us, 2), "algorithmic_bytes": nbytes,
+                    "GBps": round(nbytes / us / 1e3, 1), "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4),
+                    "TFLOPs": round(flops / us / 1e6, 2),
+                    "mfma_frac": round(flops / us / 1e6 / MFMA_BF16_PEAK_TFLOPS, 4)}
+    return out
+
+
+def calibration_copy():
+    """A plain 256 MiB device copy, so that hardware byte counters read on
+    the same run can be scaled against a transfer of known size."""
+    import torch
+    cal = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+    cal_dst = torch.empty_like(cal)
+    cal_dst.copy_(cal)
+    torch.cuda.synchronize()
+    del cal, cal_dst
+
+
+def profile_only(eng, shape, ctx, K, first, args, log):
+    """The run rocprofv3 profiles: K = K verify blocks of the model's own
+    continuation at exactly ctx committed positions, the projection timing
+    sequences of that block shape, and the calibration copy."""
+    cont = [eng.verify(0, [])[1] for _ in range(K)]
+    for _ in range(args.profile_steps):
+        eng.rollback(0, ctx, first)
+        a, _, _ = eng.verify(0, cont)
+        assert a == K
+    gemms = projection_rates(eng, shape, K + 1)
+    calibration_copy()
+    log(f"[bench] profile run: {args.profile_steps} K={K} verify blocks at n={ctx}")
+    print(json.dumps({"profile_only": True, "k": K, "ctx": ctx, "verify_blocks": args.profile_steps,
+                      "projections": gemms}), flush=True)
+
+
+# Kernels of one layer of a T = 33 block, in dispatch order (bf16, head_dim 128,
+# d <= 4096): role and kernel name prefix.
+LAYER_ROLES = [("QKV projection", "gemm_kernel<1, 3"), ("rotary + KV append", "qkv_finish_kernel<1>"),
+               ("attention", "attn_kernel<1, 128, false>"), ("split merge", "attn_combine_kernel<1, 128>"),
+               ("O projection", "gemm_kernel<1, 3"), ("residual + norm (after O)", "resid_kernel<1, 1>"),
+               ("gate/up + SwiGLU", "gemm_swiglu_kernel<1, 2, 16>"), ("down projection", "gemm_kernel<1, 3"),
+               ("residual + norm (after down)", "resid_kernel<1, 1>")]
+
+
+def _short(name: str) -> str:
+    return name.split("(")[0].replace("void ", "").replace("ee::", "").strip()
+
+
+def _layer_starts(names):
+    """Indices i where the nine dispatches of a T = 33 layer start."""
+    n = len(LAYER_ROLES)
+    return [i for i in range(len(names) - n + 1)
+            if all(names[i + j].startswith(p) for j, (_, p) in enumerate(LAYER_ROLES))]
+
+
+def rocprof_summary(d: str):
+    """Markdown tables from rocprofv3 CSV output under directory d: kernel
+    statistics, per-role durations of T = 33 layers, the kernel-gap fraction
+    of T = 33 blocks (kernel trace), and per-role counter values (counter
+    runs).  Prints to stdout."""
+    import csv
+    import glob
+    import statistics as st
+
+    def rows_of(pat):
+        f = sorted(glob.glob(os.path.join(d, "**", pat), recursive=True))
+        return list(csv.DictReader(open(f[0]))) if f else None
+
+    stats = rows_of("*kernel_stats.csv")
+    if stats:
+        print("| kernel | calls | total ms | avg us | % |\n|---|---|---|---|---|")
+        for r in stats[:20]:
+            print(f"| `{_short(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                  f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    tr = rows_of("*kernel_trace.csv")
+    if tr:
+        tr.sort(key=lambda r: int(r["Start_Timestamp"]))
+        names = [_short(r["Kernel_Name"]) for r in tr]
+        gy = [int(r["Grid_Size_Y"]) for r in tr]
+        t0 = [int(r["Start_Timestamp"]) for r in tr]
+        t1 = [int(r["End_Timestamp"]) for r in tr]
+        starts = [i for i in _layer_starts(names) if gy[i + 1] == 33]
+        print(f"\nT = 33 layers found: {len(starts)}\n")
+        print("| role | kernel | dispatches | median us | mean us |\n|---|---|---|---|---|")
+        tot = 0.0
+        for j, (role, _) in enumerate(LAYER_ROLES):
+            v = [(t1[i + j] - t0[i + j]) / 1e3 for i in starts]
+            if v:
+                tot += st.median(v)
+                print(f"| {role} | `{names[starts[0] + j]}` | {len(v)} | {st.median(v):.2f} | {st.mean(v):.2f} |")
+        print(f"| one layer (sum of medians) | | | {tot:.2f} | |")
+        # blocks of 33 rows: stage_in_kernel .. result_out_kernel; kernels busy
+        # = the union of their intervals
+        spans, busy = [], []
+        i = 0
+        while i < len(names):
+            if names[i] != "stage_in_kernel":
+                i += 1
+                continue
+            j = i
+            while j < len(names) and names[j] != "result_out_kernel":
+                j += 1
+            if j < len(names) and any(names[x] == "qkv_finish_kernel<1>" and gy[x] == 33 for x in range(i, j)):
+                b, cur_end = 0, t0[i]
+                for x in range(i, j + 1):
+                    s0, s1 = max(t0[x], cur_end), t1[x]
+                    if s1 > s0:
+                        b += s1 - s0
+                        cur_end = s1
+                spans.append((t1[j] - t0[i]) / 1e3)
+                busy.append(b / 1e3)
+            i = j + 1
+        if spans:
+            fr = [1 - b / s for b, s in zip(busy, spans)]
+            print(f"\nT = 33 blocks: {len(spans)}; first kernel start to last kernel end: median "
+                  f"{st.median(spans):.1f} us, of which kernels run {st.median(busy):.1f} us; "
+                  f"kernel-gap fraction median {st.median(fr):.4f}")
+    pmc = rows_of("*counter_collection.csv")
+    if pmc:
+        by = {}
+        for r in pmc:
+            by.setdefault(int(r["Dispatch_Id"]), []).append(r)
+        ids = sorted(by)
+        names = [_short(by[i][0]["Kernel_Name"]) for i in ids]
+        counters = sorted({r["Counter_Name"] for r in pmc})
+
+        def val(i, c):
+            return sum(float(r["Counter_Value"]) for r in by[i] if r["Counter_Name"] == c)
+        cal = [i for i in ids if "copyBuffer" in by[i][0]["Kernel_Name"]]
+        if cal:
+            big = max(cal, key=lambda i: int(by[i][0]["Grid_Size"]))
+            print("\ncalibration copy (256 MiB read, 256 MiB written): " +
+                  ", ".join(f"{c} {val(big, c):.1f}" for c in counters))
+        starts = _layer_starts(names)
+        print(f"\nT = 33 layers found: {len(starts)} (mean per dispatch)\n")
+        print("| role | " + " | ".join(counters) + " |\n|---|" + "---|" * len(counters))
+        for j, (role, _) in enumerate(LAYER_ROLES):
+            if starts:
+                print(f"| {role} | " + " | ".join(f"{st.mean(val(ids[k + j], c) for k in starts):.1f}"
+                                                  for c in counters) + " |")
+        lm = [k for k in range(len(names) - 1)
+              if names[k].startswith("gemm_kernel<1, 3") and names[k + 1].startswith("logits_kernel")]
+        if lm:
+            print("| LM head (the GEMM before the logits kernel) | " + " | ".join(
+                f"{st.mean(val(ids[k], c) for k in lm):.1f}" for c in counters) + " |")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=20, help="timed edit tasks (whole Reuse sessions re-creating G)")
+    ap.add_argument("--warmup", type=int, default=5, help="untimed edit tasks before them")
     ap.add_argument("--config", default="7b", choices=["tiny", "1b", "7b", "33b"])
     ap.add_argument("--k", type=int, default=32)
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--gen", type=int, default=512, help="length of the greedy output re-created")
-    ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--cpu-steps", type=int, default=3, help="whole K-token oracle verify steps timed")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="only fixed-context verify steps and the projection timing sequences (for rocprofv3)")
+    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--rocprof-summary", metavar="DIR", help="reduce rocprofv3 CSV output in DIR to tables")
     ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
     ap.add_argument("--no-33b", action="store_true", help="skip the 33B batch-of-4 measurement")
     ap.add_argument("--no-long", action="store_true", help="skip the long-draft (K = 128..512) measurement")
     ap.add_argument("--no-edit", action="store_true", help="skip the edit sessions with a draft model")
     args = ap.parse_args()
+    if args.rocprof_summary:
+        rocprof_summary(args.rocprof_summary)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -316,6 +511,9 @@ def main():
 
     prompt = zipf_tokens(shape.vocab, ctx, seed=42)
     first = eng.prefill(0, prompt)
+    if args.profile_only:
+        profile_only(eng, shape, ctx, K, first, args, log)
+        return
     G = [first]
     for _ in range((args.gen if args.no_long else max(args.gen, LONG_K + 1)) - 1):
         G.append(eng.verify(0, [])[1])
@@ -325,41 +523,41 @@ def main():
     code = code.tolist()
     log(f"[bench] prompt + {args.gen}-token greedy output ready at {time.perf_counter() - t0:.1f}s")
 
-    state = {}
-
-    def reset():
+    def edit_task(lat=None):
+        """One whole Reuse session re-creating G: (verify calls, emitted tokens)."""
         eng.rollback(0, ctx, first)
-        state.update(gen=[first], cursor=0)
+        gen, cur, calls, emitted = [first], 0, 0, 0
+        while len(gen) < len(G):
+            ds, _ = ee.match_reuse(gen, code, cur, MIN_NGRAM, 8)
+            start = ds if ds >= 0 else cur
+            d = code[start:start + K]
+            ts = time.perf_counter()
+            a, nxt, _ = eng.verify(0, d)
+            if lat is not None:
+                lat.append(time.perf_counter() - ts)
+            out = d[:a] + [nxt]
+            n0 = len(gen)
+            gen.extend(out)
+            m = min(len(gen), len(G))
+            if gen[n0:m] != G[n0:m]:
+                raise SystemExit(f"lossless check failed at output position {n0}")
+            cur = start + a + 1
+            calls += 1
+            emitted += len(out)
+        return calls, emitted
 
-    def reuse_step():
-        gen, cur = state["gen"], state["cursor"]
-        ds, _ = ee.match_reuse(gen, code, cur, MIN_NGRAM, 8)
-        start = ds if ds >= 0 else cur
-        d = code[start:start + K]
-        a, nxt, _ = eng.verify(0, d)
-        out = d[:a] + [nxt]
-        n0 = len(gen)
-        gen.extend(out)
-        m = min(len(gen), len(G))
-        if gen[n0:m] != G[n0:m]:
-            raise SystemExit(f"lossless check failed at output position {n0}")
-        state["cursor"] = start + a + 1
-        if len(gen) >= len(G):
-            reset()
-        return len(out)
-
-    reset()
     for _ in range(args.warmup):
-        reuse_step()
+        edit_task()
     torch.cuda.synchronize()
-    emitted, lat = 0, []
+    emitted, calls, lat = 0, 0, []
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        ts = time.perf_counter()
-        emitted += reuse_step()
-        lat.append(time.perf_counter() - ts)
+        c_, e_ = edit_task(lat)
+        calls += c_
+        emitted += e_
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    log(f"[bench] {args.steps} edit tasks: {calls} verify calls, {emitted} tokens in {elapsed:.3f}s")
 
     # dominant kernel: after the timed steps, the gate/up GEMM of the block
     # shape the session uses (T rows) is launched for each of the layers in
@@ -371,13 +569,13 @@ def main():
     gu_alg = gateup_bytes(shape, T)
 
     # verify latency at exactly `ctx` committed positions (rollback after every step)
-    def fixed_ctx(draft, parent=None, reps=60):
+    def fixed_ctx(draft, parent=None, reps=220, warm=20):
         lat, acc = [], []
         for i in range(reps):
             eng.rollback(0, ctx, first)
             ts = time.perf_counter()
             a, _, _ = eng.verify(0, draft, parent)
-            if i >= 10:
+            if i >= warm:
                 lat.append(time.perf_counter() - ts)
                 acc.append(a)
         return float(np.percentile(lat, 50)), float(np.percentile(lat, 90)), float(np.mean(acc))
@@ -406,7 +604,7 @@ def main():
     # model's own continuation, so every draft token is accepted)
     long_drafts = {}
     for kk in (() if args.no_long else (128, 256, LONG_K)):
-        l50, l90, acc = fixed_ctx(list(G_long[1:1 + kk]), reps=30)
+        l50, l90, acc = fixed_ctx(list(G_long[1:1 + kk]), reps=40, warm=10)
         e = lat_entry(kk, l50, l90, acc)
         fl = 2 * (kk + 1) * linear_weight_bytes(shape) // 2 + attention_flops(shape, kk + 1, ctx)
         e["mfma_frac"] = round(fl / l50 / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
@@ -465,20 +663,23 @@ def main():
     entropy["per_step_ms_greedy"] = select_ms(lambda: eng.verify(0, d_topk))
     eng.rollback(0, ctx, first)
 
-    # a plain device copy of known size, so that hardware byte counters read on
-    # this run can be scaled against it
-    cal = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
-    cal_dst = torch.empty_like(cal)
-    cal_dst.copy_(cal)
-    torch.cuda.synchronize()
-    del cal, cal_dst
+    gemms = projection_rates(eng, shape, T)
+    # the streaming-read rate this GPU reaches (a 2 GiB buffer, well past the
+    # 256 MB Infinity Cache)
+    sbuf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    stream_us = eng.time_stream_read(sbuf, reps=10)
+    stream_gbps = sbuf.numel() / stream_us / 1e3
+    del sbuf
+    calibration_copy()
 
     # per-class breakdown of one step (separate pass, every class instrumented)
     eng.profile(list(ee.PROF_CLASSES))
     for _ in range(10):
         eng.rollback(0, ctx, first)
         eng.verify(0, d)
-    brk = {c: round(ms / 10, 4) for c, (ms, n) in eng.profile_read(reset=True).items() if n}
+    prof = eng.profile_read(reset=True)
+    brk = {c: round(ms / 10, 4) for c, (ms, n) in prof.items() if n}
+    brk_launches = {c: n // 10 for c, (ms, n) in prof.items() if n}
     eng.profile([])
     eng.rollback(0, ctx, first)
 
@@ -503,10 +704,21 @@ def main():
                          f"{args.gen}-token greedy output, after a {ctx}-token Zipf prompt"),
             "k": K, "prompt_tokens": ctx, "regenerated_tokens": args.gen, "batch": 1,
         },
+        "step": "one edit task: the whole Reuse session re-creating the regenerated tokens",
         "emitted_per_step": round(emitted / args.steps, 3),
-        "verify_latency_ms_at_ctx": {"ctx": ctx, "p50": round(p50 * 1e3, 4), "p90": round(p90 * 1e3, 4)},
+        "verify_calls_per_step": round(calls / args.steps, 3),
+        "emitted_per_verify": round(emitted / calls, 3),
+        "ms_per_verify": {"mean": round(elapsed / calls * 1e3, 4), "p50": round(float(np.percentile(lat, 50)) * 1e3, 4),
+                          "p90": round(float(np.percentile(lat, 90)) * 1e3, 4)},
+        "verify_latency_ms_at_ctx": {"ctx": ctx, "k": K, "calls": 200, "warmup_calls": 20,
+                                     "p50": round(p50 * 1e3, 4), "p90": round(p90 * 1e3, 4)},
+        "draft_tokens_checked_per_s_at_ctx": round(K / p50, 1),
+        "full_acceptance_tokens_per_s_at_ctx": round((K + 1) / p50, 1),
         "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
-                     "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4)},
+                     "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4),
+                     "streaming_read_GBps": round(stream_gbps, 1),
+                     "frac_of_streaming_read": round(sb["total"] / p50 / 1e9 / stream_gbps, 4)},
+        "projections": gemms,
         "roofline": {
             "kernel": f"gemm_swiglu_kernel<{shape.dtype}> (gate/up projection + SwiGLU, T={T})",
             "measured": ("HIP events around 5 x 32 gate/up launches (every layer's weights in turn) run back "
@@ -521,8 +733,10 @@ def main():
             "launches": int(gu_n),
             "bytes_per_launch": gu_alg,
         },
-        "breakdown_ms_per_step": brk,
-        "breakdown_note": "HIP events around every launch; each launch's figure includes ~3-4 us of event overhead",
+        "breakdown_ms_per_verify": brk,
+        "breakdown_launches_per_verify": brk_launches,
+        "breakdown_note": ("one K=32 verify at the fixed context, every launch bracketed by HIP events (each figure "
+                           "includes ~3-4 us of event overhead per launch; every launch of the block is counted)"),
         "k_sweep_at_ctx": k_sweep,
         "tree64_at_ctx": tree64,
         "long_drafts_at_ctx": long_drafts or None,
@@ -539,8 +753,7 @@ def main():
             result["other_configs"]["33b_batch4_k64_ctx4096"] = batch_config(ee, "33b", 4, 64, 4096)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
-        result["cpu_baseline"] = cpu_baseline(shape, weights, K, ctx, args.cpu_layers,
-                                              emitted / args.steps)
+        result["cpu_baseline"] = cpu_baseline(shape, weights, K, ctx, args.cpu_steps, emitted / calls)
     print(json.dumps(result), flush=True)
 
 

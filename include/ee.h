@@ -404,7 +404,8 @@ int32_t ee_profile_read(ee_ctx* ctx, double* ms, int64_t* launches, int32_t rese
 
 /* Measurement aid: the GEMM of one projection (cls = EE_PROF_QKV,
  * EE_PROF_OPROJ, EE_PROF_GATEUP or EE_PROF_DOWN) launched for every layer in
- * turn, reps times, back to back on the context's stream, on `rows` rows of
+ * turn (EE_PROF_LMHEAD: the LM head's GEMM, n_layers times), reps times, back
+ * to back on the context's stream, on `rows` rows of
  * the workspace's current activations (the launch configuration a block of
  * that many rows uses); *us_per_launch = the elapsed time between two HIP
  * events around the sequence divided by the launches.  Each launch streams

@@ -1149,8 +1149,9 @@ int32_t ee_profile_read(ee_ctx* c, double* ms, int64_t* launches, int32_t reset)
 int32_t ee_time_gemm(ee_ctx* c, uint32_t cls, int32_t rows, int32_t reps, double* us_per_launch) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
   if (!us_per_launch || reps < 1) return fail(c, EE_EINVAL, "us_per_launch must be non-NULL and reps >= 1");
-  if (cls != EE_PROF_QKV && cls != EE_PROF_OPROJ && cls != EE_PROF_GATEUP && cls != EE_PROF_DOWN)
-    return fail(c, EE_EINVAL, "class must be one of the four projections");
+  if (cls != EE_PROF_QKV && cls != EE_PROF_OPROJ && cls != EE_PROF_GATEUP && cls != EE_PROF_DOWN &&
+      cls != EE_PROF_LMHEAD)
+    return fail(c, EE_EINVAL, "class must be one of the four projections or the LM head");
   if (rows < 1 || rows > c->lay.Rmax) return fail(c, EE_EINVAL, "rows outside [1, max_seqs * (k_max + 1)]");
   hipEvent_t e0 = nullptr, e1 = nullptr;
   HIP_TRY(c, hipEventCreate(&e0));

@@ -155,7 +155,8 @@ hipError_t run_compact(const Model& m, const Work& w, const Step& s, Prof* prof,
 // writable word (measurement aid).
 hipError_t run_stream_read(const void* buf, size_t bytes, unsigned* sink, hipStream_t st);
 // The GEMM of projection `which` (PC_QKV, PC_OPROJ, PC_GATEUP or PC_DOWN) for
-// every layer in turn, on R rows of the current activation buffers (timing).
+// every layer in turn, or the LM head's (PC_LMHEAD) as many times, on R rows
+// of the current activation buffers (timing).
 hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hipStream_t st);
 
 }  // namespace ee

@@ -2302,6 +2302,8 @@ hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hi
         break;
       case PC_DOWN: e = bf ? gemm<DT_BF16>(lp.wd, w.zbuf, d, m.F, R, w.part, st)
                            : gemm<DT_F32>(lp.wd, w.zbuf, d, m.F, R, w.part, st); break;
+      case PC_LMHEAD: e = bf ? gemm<DT_BF16>(m.lm_head, w.xbuf, m.V, d, R, w.part, st)
+                             : gemm<DT_F32>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); break;
       default: break;
     }
     if (e != hipSuccess) return e;
