@@ -75,7 +75,7 @@ struct Layout {
   size_t embed, lm_head, final_gain, layers0, per_layer, l_wqkv, l_wo, l_wgu, l_wd, l_again, l_fgain,
       packed_total;
   // workspace
-  size_t h, ssq, xbuf, zbuf, q, part, gpart, logits, amax, greedy, verdict, rowstat, ebuf, result, stage, rope, ws_total;
+  size_t h, ssq, xbuf, x2buf, ssqt, zbuf, q, part, gpart, logits, amax, greedy, verdict, rowstat, ebuf, result, stage, rope, ws_total;
   // staging sub-offsets (relative to `stage`)
   size_t s_tok, s_pos, s_prow, s_slot, s_path, s_ptable, s_info, s_eps, s_unif, s_sparam, stage_bytes;
   size_t kv_layer, kv_total;
@@ -179,6 +179,8 @@ Layout make_layout(const ee_model_config* c) {
   L.h = o; o += up(L.Rmax * d * 4);
   L.ssq = o; o += up((size_t)L.Rmax * 8 * 4);
   L.xbuf = o; o += up(Tpad * xcols * esz);
+  L.x2buf = o; o += up(Tpad * d * esz);
+  L.ssqt = o; o += up((size_t)L.Rmax * (d / 16) * 4);
   L.zbuf = o; o += up(Tpad * F * esz);
   L.q = o; o += up(L.Rmax * H * hd * esz);
   L.part = o; o += up((size_t)L.max_splits * Hkv * L.Rmax * L.G * (hd + 2) * 4);
@@ -282,6 +284,8 @@ void bind_work(ee_ctx* c) {
   w.h = reinterpret_cast<float*>(ws + L.h);
   w.ssq = reinterpret_cast<float*>(ws + L.ssq);
   w.xbuf = reinterpret_cast<uint4*>(ws + L.xbuf);
+  w.x2buf = reinterpret_cast<uint4*>(ws + L.x2buf);
+  w.ssqt = reinterpret_cast<float*>(ws + L.ssqt);
   w.zbuf = reinterpret_cast<uint4*>(ws + L.zbuf);
   w.q = ws + L.q;
   w.attn_part = reinterpret_cast<float*>(ws + L.part);

@@ -63,6 +63,9 @@ struct Work {
   float* h;                 // [Rmax, d] residual stream
   float* ssq;               // [Rmax, 8] sums of h^2 over 1024-column chunks (the norms' row scales)
   uint4* xbuf;              // packed activations, max(d, H*hd) columns
+  uint4* x2buf;             // packed activations, d columns (the FFN-side norm's output when
+                            // the O projection applies the residual and norm itself)
+  float* ssqt;              // [Rmax, d / 16] sums of h^2 per 16-column tile (that norm's row scales)
   uint4* zbuf;              // packed activations, F columns
   void* q;                  // [Rmax, H, hd] model dtype
   float* attn_part;         // [splits][Hkv][Rmax*G][hd + 2]

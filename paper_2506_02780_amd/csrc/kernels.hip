@@ -171,6 +171,14 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 8-byte buffer load (as bload).
+template <int AUX>
+__device__ __forceinline__ uint2 bload64(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
+  return make_uint2(v.x, v.y);
+}
+
 struct GemmArgs {
   const uint4* w;       // packed weights [n_tiles][S][64]
   const uint4* x;       // packed activations of all Ttot rows [ceil(Ttot/16)][S][64]
@@ -409,11 +417,46 @@ struct FkArgs {
   int S, n_pairs;     // super-steps of d; F / 16
   int R, P, z_S;      // rows; workgroups per row group; super-steps of F
   const float* ssq;   // the norm's chunk sums of h^2 ([R][8]): row scales
+  const float* ssqt;  // or (TS) its sums of h^2 per 16-column tile ([R][d / 16])
   int d;
   float eps;
 };
 
-template <int DT, int MTV, int SPW>
+// Row scales 1 / sqrt(sum h^2 / d + eps) of a row group from per-tile sums of
+// h^2 (ssqt[row][tile], d / 16 tiles of 16 columns), summed in a fixed order:
+// wave w takes rows w, w + 8, ...; lane j adds the four tile sums 4j .. 4j + 3
+// (one 16-byte load, a row's sums read by a wave in one coalesced request),
+// then an xor butterfly over the 64 lanes.  ts_load issues the loads (early),
+// ts_finish writes the scales of rows 0 .. T-1 to rsl[].
+constexpr int TS_ROWS = 5;   // rows per wave: ceil(33 / 8)
+struct TileSums {
+  float4 v[TS_ROWS];
+};
+__device__ __forceinline__ void ts_load(TileSums& t, const float* ssqt, int R, int d, int row0, int T) {
+  const int ntile = d / 16;
+  const auto r = make_rsrc(ssqt, (unsigned)((size_t)R * ntile * 4));
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < TS_ROWS; ++i) {
+    const int row = wv + 8 * i;
+    const uint4 u = bload<0>(r, (row < T && 4 * lane < ntile) ? (unsigned)(((size_t)(row0 + row) * ntile + 4 * lane) * 4)
+                                                               : OOB);
+    t.v[i] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
+  }
+}
+__device__ __forceinline__ void ts_finish(const TileSums& t, int d, float eps, int T, float* rsl) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < TS_ROWS; ++i) {
+    const int row = wv + 8 * i;
+    float s = ((t.v[i].x + t.v[i].y) + t.v[i].z) + t.v[i].w;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
+    if (lane == 0 && row < T) rsl[row] = 1.0f / sqrtf(s / (float)d + eps);
+  }
+}
+
+template <int DT, int MTV, int SPW, bool TS>
 __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, c = lane & 15, grp = lane >> 4;
   const int rg = blockIdx.x / a.P, g = blockIdx.x - rg * a.P;
@@ -432,15 +475,19 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   const int qq = threadIdx.x % (NR * 64);
   const bool qown = threadIdx.x < NR * 64;
   const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
-  // the chunk sums of the norm's row scale, requested first (memory counters
-  // complete in order) and used only in the epilogue
+  // the chunk sums (or tile sums) of the norm's row scale, requested first
+  // (memory counters complete in order) and used only in the epilogue
   RowSsq rsq;
-  {
+  TileSums tsum;
+  __shared__ float rsl[TS ? 33 : 1];
+  if (!TS) {
     const auto sr = make_rsrc(a.ssq, (unsigned)((size_t)a.R * RES_MAX_PARTS * 4));
     const unsigned so = qown && rt < T ? (unsigned)((row0 + rt) * RES_MAX_PARTS * 4) : OOB;
     const uint4 u0 = bload<0>(sr, so), u1 = bload<0>(sr, so == OOB ? OOB : so + 16);
     rsq.a = make_float4(__uint_as_float(u0.x), __uint_as_float(u0.y), __uint_as_float(u0.z), __uint_as_float(u0.w));
     rsq.b = make_float4(__uint_as_float(u1.x), __uint_as_float(u1.y), __uint_as_float(u1.z), __uint_as_float(u1.w));
+  } else {
+    ts_load(tsum, a.ssqt, a.R, a.d, row0, T);
   }
   uint4 xr[SPW][MTV];
 #pragma unroll
@@ -489,6 +536,8 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
   }
   if (rowx_own) rowx[it] = rowv;
+  // (the tile sums were requested before the inputs: they are in by now)
+  if (TS) ts_finish(tsum, a.d, a.eps, T, rsl);
   __syncthreads();
   f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < ntile; ++k) {
@@ -537,7 +586,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     } else if (qown && rt < T) {
       // features 16p + 4(rl / 16) .. +3 of row row0 + rt
       const int f = 16 * (g + (k >> 1) * a.P) + 4 * (rl >> 4);
-      const float rs = row_scale_of(rsq, a.d, a.eps);   // the norm's row scale
+      const float rs = TS ? rsl[rt] : row_scale_of(rsq, a.d, a.eps);   // the norm's row scale
       float zv[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) zv[r] = silu_mul(gate[r] * rs, v[r] * rs);
@@ -552,26 +601,28 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   }
 }
 
-template <int DT, int MTV>
+template <int DT, int MTV, bool TS>
 static void launch_gemm_swiglu(const FkArgs& a, int spw, dim3 grid, hipStream_t st) {
   const dim3 block(GEMM_WAVES * 64);
   switch (spw) {
-    case 1: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 1>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 2>), grid, block, 0, st, a); break;
-    case 4: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 4>), grid, block, 0, st, a); break;
-    case 8: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 8>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 16>), grid, block, 0, st, a); break;
+    case 1: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 1, TS>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 2, TS>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 4, TS>), grid, block, 0, st, a); break;
+    case 8: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 8, TS>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_swiglu_kernel<DT, MTV, 16, TS>), grid, block, 0, st, a); break;
   }
 }
 
-// z = silu(r x Wg^T) * (r x Wu^T) for R rows (r: each row's norm scale), when
-// d / KS <= FK_MAX_S.
+// z = silu(r x Wg^T) * (r x Wu^T) for R rows (r: each row's norm scale, from
+// 1024-column chunk sums ssq, or from 16-column tile sums ssqt when given),
+// when d / KS <= FK_MAX_S.
 template <int DT>
 static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, int R, void* z, const float* ssq,
-                              float eps, hipStream_t st) {
+                              const float* ssqt, float eps, hipStream_t st) {
   FkArgs a;
   a.w = wgu; a.x = x; a.z = z;
-  a.ssq = ssq; a.d = d; a.eps = eps;
+  a.ssq = ssq; a.ssqt = ssqt; a.d = d; a.eps = eps;
+  if (ssqt && (d % 64 || d / 64 > 64)) return hipErrorInvalidValue;
   a.S = d / Geo<DT>::KS;
   a.n_pairs = F / 16;
   a.R = R;
@@ -582,12 +633,379 @@ static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, in
   const int ng = fk_groups(R);
   a.P = ng == 1 ? std::max(1, std::min(256, a.n_pairs)) : std::max(8, 256 / ng / 8 * 8);
   const dim3 grid(ng * a.P);
-  if (R <= 16) launch_gemm_swiglu<DT, 1>(a, spw, grid, st);
-  else launch_gemm_swiglu<DT, 2>(a, spw, grid, st);
+  if (ssqt) {
+    if (R <= 16) launch_gemm_swiglu<DT, 1, true>(a, spw, grid, st);
+    else launch_gemm_swiglu<DT, 2, true>(a, spw, grid, st);
+  } else {
+    if (R <= 16) launch_gemm_swiglu<DT, 1, false>(a, spw, grid, st);
+    else launch_gemm_swiglu<DT, 2, false>(a, spw, grid, st);
+  }
   return hipGetLastError();
 }
 
 inline bool fused_swiglu(int d, int dt) { return d / ks_of(dt) <= FK_MAX_S; }
+
+// ------------------------------------------------ projection + epilogue --
+//
+// The QKV and O projections without K slices, the same loop as the gate/up
+// kernel above (a workgroup reduces its tiles over the whole of K, rows 0..31
+// in registers and the 33rd from LDS, 32-row groups for longer blocks), with
+// the kernel that followed each of them folded into the epilogue:
+//   * EP_ROPE (QKV): a workgroup owns pairs of tiles holding features i and
+//     i + hd/2 of one head (tiles j and j + hd/32 of the head); the epilogue
+//     applies the norm's row scale, rotates q and k at the row's position,
+//     stores q and appends k and v to the row's KV-pool slot;
+//   * EP_RESID (O): a workgroup owns single tiles; the epilogue adds the
+//     projection to the residual stream, stores x = h * gain of the FFN-side
+//     norm (the gate/up projection's packed input) and each row's sum of h^2
+//     over the tile's 16 columns (the row scale's tile sums).
+// Each output's reduction order depends only on K, never on the block's rows.
+
+enum { EP_ROPE = 1, EP_RESID = 2 };
+
+struct EpArgs {
+  const uint4* w;        // packed weights [n_tiles][S][64]
+  const uint4* x;        // packed activations of all R rows
+  int S, n_tiles, n_items;   // super-steps of K; 16-feature tiles; pairs (ROPE) or tiles (RESID)
+  int R, P;              // rows; workgroups per row group
+  const float* ssq;      // ROPE: the input norm's 1024-column chunk sums [R][8]
+  int d;                 // the norm's width
+  float eps;
+  // EP_ROPE
+  int H, Hkv, hd;
+  const int* pos;        // [R] rotary position of each row
+  const float2* rope;    // [max_ctx][hd / 2] (cos, sin)
+  const int* rowslot;    // [R] KV-pool slot
+  void* q;               // [R][H][hd]
+  void* kv_layer;        // this layer's KV pool (null: no K/V stores, for timing)
+  void* kv_cap;          // test aid: the block's k and v rows, or null
+  // EP_RESID
+  float* h;              // [R][d] residual stream
+  const float* gain;     // FFN-side norm gain [d]
+  void* xout;            // packed [R][d] output x = h * gain
+  int x_S;               // super-steps of d
+  float* ssqt;           // [R][n_tiles] per-tile sums of h^2
+};
+
+template <int DT, int MTV, int SPW, int EPI>
+__global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_ep_kernel(EpArgs a) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, c = lane & 15, grp = lane >> 4;
+  const int rg = blockIdx.x / a.P, g = blockIdx.x - rg * a.P;
+  const int ngroups = fk_groups(a.R);
+  const int row0 = rg * FK_GROUP;
+  const int T = rg == ngroups - 1 ? a.R - row0 : FK_GROUP;   // rows of this group, <= 33
+  const bool rowl = MTV == 2 && T > 2 * 16;                  // the 33rd row, from LDS
+  const int S = a.S;
+  constexpr int NR = MTV == 2 ? 3 : 1;                       // reduced fragment tiles
+  constexpr int ESZ = Geo<DT>::ESZ;
+  const auto xs = make_rsrc(a.x, (unsigned)((size_t)((a.R + 15) / 16) * S * 1024));
+  const auto ws = make_rsrc(a.w, (unsigned)((size_t)a.n_tiles * S * 1024));
+  __shared__ uint4 rowx[MTV == 2 ? SPW * GEMM_WAVES * 4 : 1];   // [super-step][grp]: the 33rd row
+  __shared__ f32x4 red[2][GEMM_WAVES][NR][64];
+  const int qq = threadIdx.x % (NR * 64);
+  const bool qown = threadIdx.x < NR * 64;
+  const int rm = qq >> 6, rl = qq & 63, rt = rm * 16 + (rl & 15);
+  const bool mine = qown && rt < T;                          // this thread stores row row0 + rt
+  const int row = row0 + rt;
+  // values used only in the epilogue, requested first: the rotary case's row
+  // scale (chunk sums) and the group's positions and KV slots (kept in LDS,
+  // as are the (cos, sin) of an item's features, so that the loop carries no
+  // registers for them)
+  RowSsq rsq;
+  __shared__ int spos[EPI == EP_ROPE ? FK_GROUP + 1 : 1], sslot[EPI == EP_ROPE ? FK_GROUP + 1 : 1];
+  __shared__ float2 scs[EPI == EP_ROPE ? FK_GROUP + 1 : 1][16];
+  __shared__ float srs[EPI == EP_ROPE ? FK_GROUP + 1 : 1];
+  int gpos = 0, gslot = 0;   // thread t < T: row row0 + t
+  if (EPI == EP_ROPE) {
+    const auto sr = make_rsrc(a.ssq, (unsigned)((size_t)a.R * RES_MAX_PARTS * 4));
+    const unsigned so = mine ? (unsigned)(row * RES_MAX_PARTS * 4) : OOB;
+    const uint4 u0 = bload<0>(sr, so), u1 = bload<0>(sr, so == OOB ? OOB : so + 16);
+    rsq.a = make_float4(__uint_as_float(u0.x), __uint_as_float(u0.y), __uint_as_float(u0.z), __uint_as_float(u0.w));
+    rsq.b = make_float4(__uint_as_float(u1.x), __uint_as_float(u1.y), __uint_as_float(u1.z), __uint_as_float(u1.w));
+    const auto pr = make_rsrc(a.pos, (unsigned)(a.R * 4));
+    const auto lr = make_rsrc(a.rowslot, (unsigned)(a.R * 4));
+    const bool tr = (int)threadIdx.x < T;
+    gpos = (int)__builtin_amdgcn_raw_buffer_load_b32(pr, tr ? (unsigned)((row0 + threadIdx.x) * 4) : OOB, 0, 0);
+    gslot = (int)__builtin_amdgcn_raw_buffer_load_b32(lr, tr ? (unsigned)((row0 + threadIdx.x) * 4) : OOB, 0, 0);
+  }
+  uint4 xr[SPW][MTV];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int sl = wv + GEMM_WAVES * i;
+#pragma unroll
+    for (int m = 0; m < MTV; ++m)
+      if (MTV == 2)
+        xr[i][m] = bload<0>(xs, (sl < S && m * 16 + c < min(T, 2 * 16))
+                                    ? (unsigned)((((row0 / 16 + m) * S + sl) * 64 + lane) * 16) : OOB);
+  }
+  static_assert(SPW * GEMM_WAVES * 4 <= GEMM_WAVES * 64, "one rowx entry per thread");
+  const int it = threadIdx.x;
+  const bool rowx_own = MTV == 2 && it < SPW * GEMM_WAVES * 4;
+  const uint4 rowv = bload<0>(xs, (rowx_own && rowl && (it >> 2) < S)
+                                      ? (unsigned)((((row0 / 16 + 2) * S + (it >> 2)) * 64 + (it & 3) * 16) * 16)
+                                      : OOB);
+  // items of this workgroup: g, g + P, ...; a pair is two tiles (k even: the
+  // head's first half, k odd: its second half), a RESID item one tile
+  constexpr int TPI = EPI == EP_ROPE ? 2 : 1;                // tiles per item
+  const int nitem = g < a.n_items ? (a.n_items - g + a.P - 1) / a.P : 0;
+  const int ntile = TPI * nitem;
+  const int th = a.hd / 16, hp = th / 2;                     // tiles and pairs per head
+  auto item_of = [&](int k) { return g + (k / TPI) * a.P; };
+  auto tile_of = [&](int k) {
+    if (EPI == EP_RESID) return item_of(k);
+    const int p = item_of(k);
+    return (p / hp) * th + p % hp + (k & 1) * hp;
+  };
+  auto wload = [&](int k, int i) {
+    const int sl = wv + GEMM_WAVES * i;
+    return bload<2>(ws, (k < ntile && sl < S) ? (unsigned)(((tile_of(k) * S + sl) * 64 + lane) * 16) : OOB);
+  };
+  constexpr int HA = (SPW + 1) / 2, HB = SPW / 2;            // weight halves of a tile
+  uint4 wa[HA], wb[HB > 0 ? HB : 1];
+  if (MTV == 1) {
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int sl = wv + GEMM_WAVES * i;
+      xr[i][0] = bload<0>(xs, (sl < S && c < T) ? (unsigned)((((row0 / 16) * S + sl) * 64 + lane) * 16) : OOB);
+      if (i < HA) wa[i] = wload(0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < HA; ++i) wa[i] = wload(0, i);
+  }
+  if (rowx_own) rowx[it] = rowv;
+  // the input norm's row scales (their chunk sums were requested first: they
+  // are in by now), positions and slots of the group's rows to LDS
+  if (EPI == EP_ROPE) {
+    if (mine && (rl >> 4) == 0) srs[rt] = row_scale_of(rsq, a.d, a.eps);
+    if ((int)threadIdx.x < T) {
+      spos[threadIdx.x] = gpos;
+      sslot[threadIdx.x] = gslot;
+    }
+  }
+  __syncthreads();
+  f32x4 first = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < ntile; ++k) {
+    // the epilogue's operands of this item, requested before its weights:
+    // (cos, sin) of the thread's four features (ROPE), or the residual row
+    // and gains of its four columns (RESID)
+    uint4 ep0 = make_uint4(0u, 0u, 0u, 0u), ep1 = ep0;
+    uint2 cs0 = make_uint2(0u, 0u), cs1 = cs0;   // ROPE: (cos, sin) of rows t / 16 and 32, feature t % 16
+    if (k % TPI == 0) {
+      const int f4 = 4 * (rl >> 4);
+      if (EPI == EP_ROPE) {
+        const int i0 = 16 * (item_of(k) % hp);                // the pair's first feature in the head
+        const auto cr = make_rsrc(a.rope, (unsigned)0x7fffffff);
+        const int r0 = (int)(threadIdx.x >> 4), j = (int)(threadIdx.x & 15);
+        cs0 = bload64<0>(cr, r0 < T ? (unsigned)(((size_t)spos[r0] * (a.hd / 2) + i0 + j) * 8) : OOB);
+        if (MTV == 2)
+          cs1 = bload64<0>(cr, (threadIdx.x < 16 && T > 32) ? (unsigned)(((size_t)spos[32] * (a.hd / 2) + i0 + j) * 8)
+                                                            : OOB);
+      } else {
+        const int f = 16 * item_of(k) + f4;
+        const auto hr = make_rsrc(a.h, (unsigned)((size_t)a.R * a.d * 4));
+        const auto gr = make_rsrc(a.gain, (unsigned)(a.d * 4));
+        ep0 = bload<0>(hr, mine ? (unsigned)(((size_t)row * a.d + f) * 4) : OOB);
+        ep1 = bload<0>(gr, mine ? (unsigned)(f * 4) : OOB);
+      }
+    }
+    f32x4 acc[NR];
+#pragma unroll
+    for (int m = 0; m < NR; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int RG = MTV == 2 ? (EPI == EP_ROPE ? 2 : 4) : (HA > 0 ? HA : 1);   // (ROPE: fewer registers)
+    auto steps = [&](const uint4* wf, int i0, int n) {
+#pragma unroll
+      for (int g0 = 0; g0 < n; g0 += RG) {
+        uint4 rv[RG];
+#pragma unroll
+        for (int j = 0; j < RG; ++j)
+          if (MTV == 2 && g0 + j < n) {
+            const uint4 r = rowx[(wv + GEMM_WAVES * (i0 + g0 + j)) * 4 + grp];
+            rv[j] = c == 0 ? r : make_uint4(0u, 0u, 0u, 0u);
+          }
+#pragma unroll
+        for (int j = 0; j < RG; ++j)
+          if (g0 + j < n) {
+#pragma unroll
+            for (int m = 0; m < MTV; ++m) acc[m] = mma<DT>(wf[g0 + j], xr[i0 + g0 + j][m], acc[m]);
+            if (MTV == 2) acc[2] = mma<DT>(wf[g0 + j], rv[j], acc[2]);
+          }
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < HB; ++i) wb[i] = wload(k, HA + i);
+    steps(wa, 0, HA);
+#pragma unroll
+    for (int i = 0; i < HA; ++i) wa[i] = wload(k + 1, i);
+    steps(wb, HA, HB);
+    const int pb = k & 1;
+#pragma unroll
+    for (int m = 0; m < NR; ++m) red[pb][wv][m][lane] = acc[m];
+    __syncthreads();
+    f32x4 v = red[pb][0][rm][rl];
+#pragma unroll
+    for (int j = 1; j < GEMM_WAVES; ++j) v += red[pb][j][rm][rl];
+    if (EPI == EP_ROPE && !(k & 1)) {
+      // the item's (cos, sin) to LDS (read after the next barrier)
+      first = v;
+      const int r0 = (int)(threadIdx.x >> 4), j = (int)(threadIdx.x & 15);
+      if (r0 < T) scs[r0][j] = make_float2(__uint_as_float(cs0.x), __uint_as_float(cs0.y));
+      if (MTV == 2 && threadIdx.x < 16 && T > 32) scs[32][j] = make_float2(__uint_as_float(cs1.x), __uint_as_float(cs1.y));
+    } else if (EPI == EP_ROPE && mine) {
+      const int p = item_of(k), head = p / hp, f4 = 4 * (rl >> 4), i0 = 16 * (p % hp) + f4, half = a.hd / 2;
+      const float rs = srs[rt];
+      float cs[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float2 v2 = scs[rt][f4 + r];
+        cs[2 * r] = v2.x;
+        cs[2 * r + 1] = v2.y;
+      }
+      const int myslot = sslot[rt];
+      float y1[4], y2[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x1 = first[r] * rs, x2 = v[r] * rs;
+        if (head < a.H + a.Hkv) {
+          y1[r] = x1 * cs[2 * r] - x2 * cs[2 * r + 1];
+          y2[r] = x2 * cs[2 * r] + x1 * cs[2 * r + 1];
+        } else {
+          y1[r] = x1;
+          y2[r] = x2;
+        }
+      }
+      // stores through 32-bit buffer offsets (q, one KV-pool layer and the
+      // capture stay below 2 GiB)
+      auto put4 = [&](__amdgpu_buffer_rsrc_t r, unsigned e, const float* y) {
+        if (DT == DT_BF16) {
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          __builtin_amdgcn_raw_buffer_store_b64(
+              u32x2{f2bf_bits(y[0]) | (f2bf_bits(y[1]) << 16), f2bf_bits(y[2]) | (f2bf_bits(y[3]) << 16)}, r,
+              e * 2, 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b128(
+              u32x4{__float_as_uint(y[0]), __float_as_uint(y[1]), __float_as_uint(y[2]), __float_as_uint(y[3])}, r,
+              e * 4, 0, 0);
+        }
+      };
+      auto put1 = [&](__amdgpu_buffer_rsrc_t r, unsigned e, float y) {
+        if (DT == DT_BF16)
+          __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf_bits(y), r, e * 2, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), r, e * 4, 0, 0);
+      };
+      const unsigned layer_bytes = 0x7fffffffu;   // (the pool layer is below 2 GiB: checked at creation)
+      const int page = myslot >> 6, sp = myslot & 63;
+      // the row's address terms are formed here, not kept through the loop
+      int row = row0 + rt;
+      asm volatile("" : "+v"(row));
+      if (head < a.H) {
+        const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.R * a.H * a.hd * ESZ));
+        const unsigned qb = ((unsigned)row * a.H + head) * a.hd;
+        put4(qr, qb + i0, y1);
+        put4(qr, qb + i0 + half, y2);
+      } else if (head < a.H + a.Hkv) {
+        const int kh = head - a.H;
+        if (a.kv_layer) {
+          const auto kr = make_rsrc(a.kv_layer, layer_bytes);
+          const unsigned kb = (((unsigned)page * 2 + 0) * a.Hkv + kh) * 64 * a.hd + (unsigned)sp * a.hd;
+          put4(kr, kb + i0, y1);
+          put4(kr, kb + i0 + half, y2);
+        }
+        if (a.kv_cap) {   // test aid: the block's k rows, [R][Hkv][hd]
+          const auto cr = make_rsrc(a.kv_cap, (unsigned)((size_t)2 * a.R * a.Hkv * a.hd * ESZ));
+          const unsigned cb = ((unsigned)row * a.Hkv + kh) * a.hd;
+          put4(cr, cb + i0, y1);
+          put4(cr, cb + i0 + half, y2);
+        }
+      } else {
+        const int vh = head - a.H - a.Hkv;
+        if (a.kv_layer) {
+          const auto vr = make_rsrc(a.kv_layer, layer_bytes);
+          const unsigned vb = (((unsigned)page * 2 + 1) * a.Hkv + vh) * 64 * a.hd;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            put1(vr, vb + (unsigned)(i0 + r) * 64 + sp, y1[r]);
+            put1(vr, vb + (unsigned)(i0 + r + half) * 64 + sp, y2[r]);
+          }
+        }
+        if (a.kv_cap) {   // test aid: the block's v rows after the k rows
+          const auto cr = make_rsrc(a.kv_cap, (unsigned)((size_t)2 * a.R * a.Hkv * a.hd * ESZ));
+          const unsigned cb = ((unsigned)a.R * a.Hkv + (unsigned)row * a.Hkv + vh) * a.hd;
+          put4(cr, cb + i0, y1);
+          put4(cr, cb + i0 + half, y2);
+        }
+      }
+    } else if (EPI == EP_RESID) {
+      // residual add, x = h * gain (bf16 for the next projection), and the
+      // row's sum of h^2 over this tile's 16 columns (four lanes of 4 columns,
+      // added by an xor butterfly: every lane gets the same value)
+      const int tile = item_of(k), f = 16 * tile + 4 * (rl >> 4);
+      const float hv[4] = {__uint_as_float(ep0.x), __uint_as_float(ep0.y), __uint_as_float(ep0.z),
+                           __uint_as_float(ep0.w)};
+      const float gn[4] = {__uint_as_float(ep1.x), __uint_as_float(ep1.y), __uint_as_float(ep1.z),
+                           __uint_as_float(ep1.w)};
+      float hn[4], xo[4], ss = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        hn[r] = hv[r] + v[r];
+        ss = fmaf(hn[r], hn[r], ss);
+        xo[r] = hn[r] * gn[r];
+      }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      if (mine) {
+        *reinterpret_cast<float4*>(a.h + (size_t)row * a.d + f) = make_float4(hn[0], hn[1], hn[2], hn[3]);
+        const size_t fi = frag_index<DT>(row, f, a.x_S);
+        if (DT == DT_BF16)
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.xout) + fi) =
+              make_uint2(f2bf_bits(xo[0]) | (f2bf_bits(xo[1]) << 16), f2bf_bits(xo[2]) | (f2bf_bits(xo[3]) << 16));
+        else
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.xout) + fi) = make_float4(xo[0], xo[1], xo[2], xo[3]);
+        if ((rl >> 4) == 0) a.ssqt[(size_t)row * a.n_tiles + tile] = ss;
+      }
+    }
+  }
+}
+
+template <int DT, int MTV, int EPI>
+static void launch_gemm_ep(const EpArgs& a, int spw, dim3 grid, hipStream_t st) {
+  const dim3 block(GEMM_WAVES * 64);
+  switch (spw) {
+    case 1: hipLaunchKernelGGL((gemm_ep_kernel<DT, MTV, 1, EPI>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_ep_kernel<DT, MTV, 2, EPI>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_ep_kernel<DT, MTV, 4, EPI>), grid, block, 0, st, a); break;
+    case 8: hipLaunchKernelGGL((gemm_ep_kernel<DT, MTV, 8, EPI>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_ep_kernel<DT, MTV, 16, EPI>), grid, block, 0, st, a); break;
+  }
+}
+
+// The projection of `a` (weights, activations, K = a.S super-steps, n_tiles,
+// the epilogue's operands filled in) for R rows with epilogue EPI.
+template <int DT, int EPI>
+static hipError_t gemm_ep(EpArgs a, int R, hipStream_t st) {
+  if (a.S > FK_MAX_S) return hipErrorInvalidValue;
+  if (EPI == EP_ROPE && (a.hd % 32 || a.n_tiles % (a.hd / 16))) return hipErrorInvalidValue;
+  a.R = R;
+  int spw = 1;
+  while (spw * GEMM_WAVES < a.S) spw *= 2;
+  const int ng = fk_groups(R);
+  a.P = ng == 1 ? std::max(1, std::min(256, a.n_items)) : std::max(8, 256 / ng / 8 * 8);
+  const dim3 grid(ng * a.P);
+  if (R <= 16) launch_gemm_ep<DT, 1, EPI>(a, spw, grid, st);
+  else launch_gemm_ep<DT, 2, EPI>(a, spw, grid, st);
+  return hipGetLastError();
+}
+
+// Whether the QKV and O projections run as gemm_ep_kernel (their reduction
+// and the gate/up projection's fit one workgroup; rotary pairs of 16-feature
+// tiles need head_dim a multiple of 32; the row scale's tile sums need d a
+// multiple of 64 and at most 4096: one 16-byte load per lane).  Depends only on the
+// model's shape.
+inline bool fused_proj(int d, int qdim, int hd, int dt) {
+  return d / ks_of(dt) <= FK_MAX_S && qdim / ks_of(dt) <= FK_MAX_S && hd % 32 == 0 && d % 64 == 0 && d <= 4096;
+}
 
 // ------------------------------------------------------------ embed / norm --
 
@@ -869,12 +1287,6 @@ struct AttnArgs {
 constexpr int SPLIT = 256;   // keys per split (4 sub-tiles of 64)
 constexpr int NSUB = SPLIT / 64;
 
-template <int AUX>
-__device__ __forceinline__ uint2 bload64(__amdgpu_buffer_rsrc_t r, unsigned off) {
-  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX);
-  return make_uint2(v.x, v.y);
-}
 
 // workgroup size: 16 waves (4 query tiles x 4 sub-tiles); the tree variant
 // runs 8 waves (2 query tiles) so that its gather loop has 256 registers
@@ -2086,11 +2498,21 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
   if (nsplit < 1 || nsplit > w.max_splits || nsplit > MAX_SPLITS) return hipErrorInvalidValue;
   const int nqt = (ncols + 15) / 16;
   const int pairs = (m.H + 2 * m.Hkv) * (m.hd / 2);
+  const bool fused = fused_proj(d, qdim, m.hd, DT);
 
   for (int l = 0; l < m.L; ++l) {
     const LayerPtrs& lp = m.layers[l];
     void* kvl = reinterpret_cast<unsigned char*>(m.kv_pool) + l * layer_elems * Geo<DT>::ESZ;
-    // QKV projection, then rotary + KV append
+    // QKV projection, then rotary + KV append (in the projection's epilogue
+    // when fused, else a kernel of their own)
+    if (fused) {
+      EpArgs qa{};
+      qa.w = lp.wqkv; qa.x = w.xbuf; qa.S = Sd; qa.n_tiles = qkvN / 16; qa.n_items = qkvN / 32;
+      qa.ssq = w.ssq; qa.d = d; qa.eps = m.eps;
+      qa.H = m.H; qa.Hkv = m.Hkv; qa.hd = m.hd; qa.pos = w.pos; qa.rope = m.rope; qa.rowslot = w.slot;
+      qa.q = w.q; qa.kv_layer = kvl; qa.kv_cap = s.cap ? (void*)(s.cap + (size_t)l * c_layer + c_k) : nullptr;
+      if ((e = timed(prof, PC_QKV, st, [&] { return gemm_ep<DT, EP_ROPE>(qa, R, st); })) != hipSuccess) return e;
+    } else {
     if ((e = timed(prof, PC_QKV, st, [&] { return gemm<DT>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_FINISH, st, [&] {
@@ -2100,6 +2522,7 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            return last();
          })) != hipSuccess)
       return e;
+    }
     if (s.cap && (e = cap(l, c_q, w.q, (size_t)R * qdim * ESZ)) != hipSuccess) return e;
     // attention
     AttnArgs aa{};
@@ -2160,7 +2583,17 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          })) != hipSuccess)
       return e;
     if (s.cap && (e = cap(l, c_o, w.xbuf, R16 * qdim * ESZ)) != hipSuccess) return e;
-    // O projection; residual add + FFN norm
+    // O projection; residual add + FFN norm (in the projection's epilogue when
+    // fused: x = h * gain into x2buf and tile sums of h^2, else a kernel of
+    // their own writing xbuf and chunk sums)
+    if (fused) {
+      EpArgs oa{};
+      oa.w = lp.wo; oa.x = w.xbuf; oa.S = Sq; oa.n_tiles = d / 16; oa.n_items = d / 16;
+      oa.d = d; oa.eps = m.eps; oa.h = w.h; oa.gain = lp.ffn_gain; oa.xout = (void*)w.x2buf; oa.x_S = Sd;
+      oa.ssqt = w.ssqt;
+      if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm_ep<DT, EP_RESID>(oa, R, st); })) != hipSuccess) return e;
+      if (s.cap && (e = cap(l, c_xf, w.x2buf, R16 * d * ESZ)) != hipSuccess) return e;
+    } else {
     if ((e = timed(prof, PC_OPROJ, st, [&] { return gemm<DT>(lp.wo, w.xbuf, d, qdim, R, w.part, st); })) != hipSuccess)
       return e;
     if ((e = timed(prof, PC_NORM, st, [&] {
@@ -2170,11 +2603,13 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
          })) != hipSuccess)
       return e;
     if (s.cap && (e = cap(l, c_xf, w.xbuf, R16 * d * ESZ)) != hipSuccess) return e;
+    }
     // gate/up projection and SwiGLU: fused for d / KS <= FK_MAX_S, else
     // split-K partials and a SwiGLU launch
     if (fused_swiglu(d, DT)) {
       if ((e = timed(prof, PC_GATEUP, st, [&] {
-             return gemm_swiglu<DT>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st);
+             return fused ? gemm_swiglu<DT>(lp.wgu, w.x2buf, m.F, d, R, (void*)w.zbuf, w.ssq, w.ssqt, m.eps, st)
+                          : gemm_swiglu<DT>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, nullptr, m.eps, st);
            })) != hipSuccess)
         return e;
     } else {
@@ -2287,15 +2722,37 @@ hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hi
     const LayerPtrs& lp = m.layers[l];
     hipError_t e = hipErrorInvalidValue;
     const bool bf = m.dt == DT_BF16;
+    const bool fused = fused_proj(d, qdim, m.hd, m.dt);
+    const int ks = ks_of(m.dt);
+    EpArgs ea{};
+    ea.d = d; ea.eps = m.eps;
+    if (which == PC_QKV) {
+      // no K/V stores (the staged slots may hold committed rows)
+      ea.w = lp.wqkv; ea.x = w.xbuf; ea.S = d / ks; ea.n_tiles = qkvN / 16; ea.n_items = qkvN / 32;
+      ea.ssq = w.ssq; ea.H = m.H; ea.Hkv = m.Hkv; ea.hd = m.hd; ea.pos = w.pos; ea.rope = m.rope;
+      ea.rowslot = w.slot; ea.q = w.q;
+    } else if (which == PC_OPROJ) {
+      ea.w = lp.wo; ea.x = w.xbuf; ea.S = qdim / ks; ea.n_tiles = d / 16; ea.n_items = d / 16;
+      ea.h = w.h; ea.gain = lp.ffn_gain; ea.xout = (void*)w.x2buf; ea.x_S = d / ks; ea.ssqt = w.ssqt;
+    }
     switch (which) {
-      case PC_QKV: e = bf ? gemm<DT_BF16>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st)
-                          : gemm<DT_F32>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st); break;
-      case PC_OPROJ: e = bf ? gemm<DT_BF16>(lp.wo, w.xbuf, d, qdim, R, w.part, st)
-                            : gemm<DT_F32>(lp.wo, w.xbuf, d, qdim, R, w.part, st); break;
+      case PC_QKV:
+        if (fused) e = bf ? gemm_ep<DT_BF16, EP_ROPE>(ea, R, st) : gemm_ep<DT_F32, EP_ROPE>(ea, R, st);
+        else e = bf ? gemm<DT_BF16>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st)
+                    : gemm<DT_F32>(lp.wqkv, w.xbuf, qkvN, d, R, w.part, st);
+        break;
+      case PC_OPROJ:
+        if (fused) e = bf ? gemm_ep<DT_BF16, EP_RESID>(ea, R, st) : gemm_ep<DT_F32, EP_RESID>(ea, R, st);
+        else e = bf ? gemm<DT_BF16>(lp.wo, w.xbuf, d, qdim, R, w.part, st)
+                    : gemm<DT_F32>(lp.wo, w.xbuf, d, qdim, R, w.part, st);
+        break;
       case PC_GATEUP:
-        if (fused_swiglu(d, m.dt))
-          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st)
-                 : gemm_swiglu<DT_F32>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, m.eps, st);
+        if (fused)
+          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.x2buf, m.F, d, R, (void*)w.zbuf, w.ssq, w.ssqt, m.eps, st)
+                 : gemm_swiglu<DT_F32>(lp.wgu, w.x2buf, m.F, d, R, (void*)w.zbuf, w.ssq, w.ssqt, m.eps, st);
+        else if (fused_swiglu(d, m.dt))
+          e = bf ? gemm_swiglu<DT_BF16>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, nullptr, m.eps, st)
+                 : gemm_swiglu<DT_F32>(lp.wgu, w.xbuf, m.F, d, R, (void*)w.zbuf, w.ssq, nullptr, m.eps, st);
         else
           e = bf ? gemm<DT_BF16>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st)
                  : gemm<DT_F32>(lp.wgu, w.xbuf, 2 * m.F, d, R, w.part, st);
