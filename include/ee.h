@@ -415,17 +415,19 @@ int32_t ee_profile_read(ee_ctx* ctx, double* ms, int64_t* launches, int32_t rese
  * another class, rows outside [1, max_seqs * (k_max + 1)] or reps < 1. */
 int32_t ee_time_gemm(ee_ctx* ctx, uint32_t cls, int32_t rows, int32_t reps, double* us_per_launch);
 
+/* Measurement aid (no paper passage: infrastructure): microseconds per pass
+ * of a plain streaming read of `bytes` (a multiple of 16, at least 256 KiB)
+ * of caller device memory at `dev_buf`, averaged over `reps` back-to-back
+ * passes on the context's stream after one untimed pass: the HBM read rate
+ * this GPU reaches in practice (one workgroup per CU, each reading a
+ * contiguous chunk), which the verify step's rate is compared with.  The
+ * buffer is only read.  EE_EINVAL for a smaller or misaligned size, a null
+ * buffer or output, or reps < 1. */
+int32_t ee_time_stream_read(ee_ctx* ctx, const void* dev_buf, size_t bytes, int32_t reps, double* us_per_pass);
+
 /* Message for the last failed call on ctx (or the last failed context-free
  * call when ctx is NULL).  Never NULL; the pointer stays valid until the next
  * call on the same context. */
-/* Measurement aid (no paper passage: infrastructure): microseconds per pass
- * of a plain streaming read of `bytes` (a multiple of 16) of caller device
- * memory at `dev_buf`, averaged over `reps` back-to-back passes on the
- * context's stream after one untimed pass: the HBM read rate this GPU
- * reaches in practice, which the verify step's rate is compared with.  The
- * buffer is only read. */
-int32_t ee_time_stream_read(ee_ctx* ctx, const void* dev_buf, size_t bytes, int32_t reps, double* us_per_pass);
-
 const char* ee_last_error(const ee_ctx* ctx);
 
 #ifdef __cplusplus

@@ -1178,8 +1178,8 @@ int32_t ee_time_gemm(ee_ctx* c, uint32_t cls, int32_t rows, int32_t reps, double
 
 int32_t ee_time_stream_read(ee_ctx* c, const void* dev_buf, size_t bytes, int32_t reps, double* us_per_pass) {
   if (!c) return fail(nullptr, EE_EINVAL, "context is NULL");
-  if (!dev_buf || !us_per_pass || reps < 1 || bytes < 16 || bytes % 16)
-    return fail(c, EE_EINVAL, "a buffer of a multiple of 16 bytes, reps >= 1 and an output are needed");
+  if (!dev_buf || !us_per_pass || reps < 1 || bytes < ((size_t)256 << 10) || bytes % 16)
+    return fail(c, EE_EINVAL, "a buffer of at least 256 KiB (a multiple of 16 bytes), reps >= 1 and an output are needed");
   hipEvent_t e0 = nullptr, e1 = nullptr;
   HIP_TRY(c, hipEventCreate(&e0));
   if (hipEventCreate(&e1) != hipSuccess) {

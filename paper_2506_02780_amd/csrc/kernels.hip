@@ -422,37 +422,55 @@ struct FkArgs {
   float eps;
 };
 
-// Row scales 1 / sqrt(sum h^2 / d + eps) of a row group from per-tile sums of
-// h^2 (ssqt[row][tile], d / 16 tiles of 16 columns), summed in a fixed order:
-// wave w takes rows w, w + 8, ...; lane j adds the four tile sums 4j .. 4j + 3
-// (one 16-byte load, a row's sums read by a wave in one coalesced request),
-// then an xor butterfly over the 64 lanes.  ts_load issues the loads (early),
-// ts_finish writes the scales of rows 0 .. T-1 to rsl[].
-constexpr int TS_ROWS = 5;   // rows per wave: ceil(33 / 8)
+// Row scales 1 / sqrt(sum h^2 / d + eps) of a row group from the per-tile sums
+// of h^2 (ssqt[row][tile], d / 16 tiles of 16 columns; d a multiple of 256 and
+// at most 4096), in a fixed order: a row's tile sums in chunks of 16 (one
+// thread adds a chunk in tile order), then its chunk sums in chunk order.
+// ts_issue requests the chunks of items threadIdx.x and threadIdx.x + 512
+// (33 rows x 16 chunks at most); ts_chunks stores their sums to LDS; after a
+// barrier, ts_rows turns each row's chunk sums into its scale.
+constexpr int TS_CHUNKS = 16;   // chunks of a row, at most
 struct TileSums {
-  float4 v[TS_ROWS];
+  uint4 v[2][4];
 };
-__device__ __forceinline__ void ts_load(TileSums& t, const float* ssqt, int R, int d, int row0, int T) {
-  const int ntile = d / 16;
+__device__ __forceinline__ void ts_issue(TileSums& t, const float* ssqt, int R, int d, int row0, int T) {
+  const int ntile = d / 16, nch = d / 256;
   const auto r = make_rsrc(ssqt, (unsigned)((size_t)R * ntile * 4));
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = 0; i < TS_ROWS; ++i) {
-    const int row = wv + 8 * i;
-    const uint4 u = bload<0>(r, (row < T && 4 * lane < ntile) ? (unsigned)(((size_t)(row0 + row) * ntile + 4 * lane) * 4)
-                                                               : OOB);
-    t.v[i] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
+  for (int p = 0; p < 2; ++p) {
+    const int item = (int)threadIdx.x + GEMM_WAVES * 64 * p, row = item / nch, ch = item - row * nch;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      t.v[p][q] = bload<0>(r, row < T ? (unsigned)(((size_t)(row0 + row) * ntile + ch * 16 + 4 * q) * 4) : OOB);
   }
 }
-__device__ __forceinline__ void ts_finish(const TileSums& t, int d, float eps, int T, float* rsl) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+__device__ __forceinline__ void ts_chunks(const TileSums& t, int d, int T, float (*tsc)[TS_CHUNKS]) {
+  const int nch = d / 256;
 #pragma unroll
-  for (int i = 0; i < TS_ROWS; ++i) {
-    const int row = wv + 8 * i;
-    float s = ((t.v[i].x + t.v[i].y) + t.v[i].z) + t.v[i].w;
+  for (int p = 0; p < 2; ++p) {
+    const int item = (int)threadIdx.x + GEMM_WAVES * 64 * p, row = item / nch, ch = item - row * nch;
+    float s = __uint_as_float(t.v[p][0].x);
+    s += __uint_as_float(t.v[p][0].y);
+    s += __uint_as_float(t.v[p][0].z);
+    s += __uint_as_float(t.v[p][0].w);
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
-    if (lane == 0 && row < T) rsl[row] = 1.0f / sqrtf(s / (float)d + eps);
+    for (int q = 1; q < 4; ++q) {
+      s += __uint_as_float(t.v[p][q].x);
+      s += __uint_as_float(t.v[p][q].y);
+      s += __uint_as_float(t.v[p][q].z);
+      s += __uint_as_float(t.v[p][q].w);
+    }
+    if (row < T) tsc[row][ch] = s;
+  }
+}
+__device__ __forceinline__ void ts_rows(const float (*tsc)[TS_CHUNKS], int d, float eps, int T, float* rsl) {
+  const int nch = d / 256, t = (int)threadIdx.x;
+  if (t < T) {
+    float s = tsc[t][0];
+#pragma unroll
+    for (int ch = 1; ch < TS_CHUNKS; ++ch)
+      if (ch < nch) s += tsc[t][ch];
+    rsl[t] = 1.0f / sqrtf(s / (float)d + eps);
   }
 }
 
@@ -479,7 +497,8 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   // (memory counters complete in order) and used only in the epilogue
   RowSsq rsq;
   TileSums tsum;
-  __shared__ float rsl[TS ? 33 : 1];
+  __shared__ float rsl[TS ? FK_GROUP + 1 : 1];
+  __shared__ float tsc[TS ? FK_GROUP + 1 : 1][TS_CHUNKS];
   if (!TS) {
     const auto sr = make_rsrc(a.ssq, (unsigned)((size_t)a.R * RES_MAX_PARTS * 4));
     const unsigned so = qown && rt < T ? (unsigned)((row0 + rt) * RES_MAX_PARTS * 4) : OOB;
@@ -487,7 +506,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
     rsq.a = make_float4(__uint_as_float(u0.x), __uint_as_float(u0.y), __uint_as_float(u0.z), __uint_as_float(u0.w));
     rsq.b = make_float4(__uint_as_float(u1.x), __uint_as_float(u1.y), __uint_as_float(u1.z), __uint_as_float(u1.w));
   } else {
-    ts_load(tsum, a.ssqt, a.R, a.d, row0, T);
+    ts_issue(tsum, a.ssqt, a.R, a.d, row0, T);
   }
   uint4 xr[SPW][MTV];
 #pragma unroll
@@ -537,8 +556,9 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_swiglu_kernel(FkArgs a) 
   }
   if (rowx_own) rowx[it] = rowv;
   // (the tile sums were requested before the inputs: they are in by now)
-  if (TS) ts_finish(tsum, a.d, a.eps, T, rsl);
+  if (TS) ts_chunks(tsum, a.d, T, tsc);
   __syncthreads();
+  if (TS) ts_rows(tsc, a.d, a.eps, T, rsl);   // (read after the first tile's barrier)
   f32x4 gate = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < ntile; ++k) {
     f32x4 acc[NR];
@@ -622,7 +642,7 @@ static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, in
   FkArgs a;
   a.w = wgu; a.x = x; a.z = z;
   a.ssq = ssq; a.ssqt = ssqt; a.d = d; a.eps = eps;
-  if (ssqt && (d % 64 || d / 64 > 64)) return hipErrorInvalidValue;
+  if (ssqt && (d % 256 || d > 4096)) return hipErrorInvalidValue;
   a.S = d / Geo<DT>::KS;
   a.n_pairs = F / 16;
   a.R = R;
@@ -868,8 +888,8 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_ep_kernel(EpArgs a) {
       for (int r = 0; r < 4; ++r) {
         const float x1 = first[r] * rs, x2 = v[r] * rs;
         if (head < a.H + a.Hkv) {
-          y1[r] = x1 * cs[2 * r] - x2 * cs[2 * r + 1];
-          y2[r] = x2 * cs[2 * r] + x1 * cs[2 * r + 1];
+          y1[r] = fmaf(x1, cs[2 * r], -(x2 * cs[2 * r + 1]));   // (fixed contraction)
+          y2[r] = fmaf(x2, cs[2 * r], x1 * cs[2 * r + 1]);
         } else {
           y1[r] = x1;
           y2[r] = x2;
@@ -1001,10 +1021,9 @@ static hipError_t gemm_ep(EpArgs a, int R, hipStream_t st) {
 // Whether the QKV and O projections run as gemm_ep_kernel (their reduction
 // and the gate/up projection's fit one workgroup; rotary pairs of 16-feature
 // tiles need head_dim a multiple of 32; the row scale's tile sums need d a
-// multiple of 64 and at most 4096: one 16-byte load per lane).  Depends only on the
-// model's shape.
+// multiple of 256 and at most 4096).  Depends only on the model's shape.
 inline bool fused_proj(int d, int qdim, int hd, int dt) {
-  return d / ks_of(dt) <= FK_MAX_S && qdim / ks_of(dt) <= FK_MAX_S && hd % 32 == 0 && d % 64 == 0 && d <= 4096;
+  return d / ks_of(dt) <= FK_MAX_S && qdim / ks_of(dt) <= FK_MAX_S && hd % 32 == 0 && d % 256 == 0 && d <= 4096;
 }
 
 // ------------------------------------------------------------ embed / norm --
@@ -1106,8 +1125,8 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(const float* __restrict
   const int page = slot >> 6, sp = slot & 63;
   if (head < H + Hkv) {
     const float2 cs = rope[(size_t)pos[t] * half + i];
-    const float y1 = x1 * cs.x - x2 * cs.y;
-    const float y2 = x2 * cs.x + x1 * cs.y;
+    const float y1 = fmaf(x1, cs.x, -(x2 * cs.y));   // (fixed contraction)
+    const float y2 = fmaf(x2, cs.x, x1 * cs.y);
     if (head < H) {
       const size_t qb = ((size_t)t * H + head) * hd;
       store_elt<DT>(q, qb + i, y1);
@@ -2421,36 +2440,47 @@ static hipError_t timed(Prof* prof, int c, hipStream_t st, F&& launch) {
 //
 // Measurement aid: the HBM read rate a plain streaming kernel reaches on this
 // part (the achievable bandwidth the verify step is also compared with).
-// Each thread keeps eight non-temporal 16-byte loads in flight; the loaded
-// words are folded into a value that is stored only in a case that does not
-// occur for the data measured (so the loads cannot be dropped).
-constexpr int STREAM_THREADS = 256, STREAM_UNROLL = 8;
+// One workgroup per CU reads a contiguous chunk of the buffer: its four waves
+// take 1 KB segments round-robin, eight non-temporal 16-byte loads in flight
+// per thread (the pattern of the GEMMs' weight streams; a grid-stride walk
+// over the whole buffer reaches about 15% less).  The loaded words are folded
+// into a value that is stored only in a case that does not occur for the data
+// measured (so the loads cannot be dropped).
+constexpr int STREAM_THREADS = 256, STREAM_UNROLL = 8, STREAM_BLOCKS = 256;
 
 __global__ __launch_bounds__(STREAM_THREADS) void stream_read_kernel(const u32x4* __restrict__ p, size_t n16,
                                                                      unsigned* __restrict__ sink) {
-  const size_t stride = (size_t)gridDim.x * STREAM_THREADS;
-  size_t i = (size_t)blockIdx.x * STREAM_THREADS + threadIdx.x;
+  constexpr int W = STREAM_THREADS / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  // chunk of this workgroup: whole 1 KB segments; the last one also takes
+  // the remainder
+  const size_t seg_all = n16 / 64, per = seg_all / gridDim.x;
+  const size_t s0 = (size_t)blockIdx.x * per, s1 = blockIdx.x + 1 == gridDim.x ? seg_all : s0 + per;
   uint32_t acc = 0;
-  for (; i + (STREAM_UNROLL - 1) * stride < n16; i += STREAM_UNROLL * stride) {
+  size_t s = s0 + wv;
+  for (; s + (size_t)(STREAM_UNROLL - 1) * W < s1; s += (size_t)STREAM_UNROLL * W) {
     u32x4 v[STREAM_UNROLL];
 #pragma unroll
-    for (int j = 0; j < STREAM_UNROLL; ++j) v[j] = __builtin_nontemporal_load(p + i + j * stride);
+    for (int j = 0; j < STREAM_UNROLL; ++j) v[j] = __builtin_nontemporal_load(p + (s + (size_t)j * W) * 64 + lane);
 #pragma unroll
     for (int j = 0; j < STREAM_UNROLL; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   }
-  for (; i < n16; i += stride) {
-    const u32x4 v = __builtin_nontemporal_load(p + i);
+  for (; s < s1; s += W) {
+    const u32x4 v = __builtin_nontemporal_load(p + s * 64 + lane);
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
+  if (blockIdx.x + 1 == gridDim.x)   // the last partial segment
+    for (size_t i = seg_all * 64 + threadIdx.x; i < n16; i += STREAM_THREADS) {
+      const u32x4 v = __builtin_nontemporal_load(p + i);
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
   if (acc == 0x9e3779b9u) sink[0] = acc;
 }
 
 hipError_t run_stream_read(const void* buf, size_t bytes, unsigned* sink, hipStream_t st) {
   const size_t n16 = bytes / 16;
-  if (n16 == 0) return hipErrorInvalidValue;
-  const size_t want = (n16 + STREAM_THREADS * STREAM_UNROLL - 1) / (STREAM_THREADS * STREAM_UNROLL);
-  const int blocks = (int)std::min<size_t>(want, 256 * 8);   // 8 workgroups per CU
-  hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(STREAM_THREADS), 0, st,
+  if (n16 < (size_t)64 * STREAM_BLOCKS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(stream_read_kernel, dim3(STREAM_BLOCKS), dim3(STREAM_THREADS), 0, st,
                      reinterpret_cast<const u32x4*>(buf), n16, sink);
   return hipGetLastError();
 }

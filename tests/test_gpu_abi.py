@@ -78,6 +78,16 @@ def test_time_gemm_measurement_aid(ee, eng):
     assert eng.seq_state(0) == n0
 
 
+def test_time_stream_read_measurement_aid(ee, eng):
+    import torch
+    buf = torch.empty((1 << 20) + 48, dtype=torch.uint8, device="cuda")   # a partial last segment
+    us = eng.time_stream_read(buf, reps=2)
+    assert 0.0 < us < 1e5
+    with pytest.raises(ee.EEError) as e:
+        eng.time_stream_read(buf[:1 << 17], reps=1)   # below 256 KiB
+    assert e.value.code == ee.EE_EINVAL
+
+
 def test_load_kv_round_trip_errors_and_parity(ee, eng):
     """ee_load_kv installs a cache that ee_read_kv returns unchanged; a block
     over it matches the oracle over the same cache (fp32, 1e-4); errors leave
