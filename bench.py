@@ -352,11 +352,12 @@ def profile_only(eng, shape, ctx, K, first, args, log):
 
 # Kernels of one layer of a T = 33 block, in dispatch order (bf16, head_dim 128,
 # d <= 4096): role and kernel name prefix.
-LAYER_ROLES = [("QKV projection", "gemm_kernel<1, 3"), ("rotary + KV append", "qkv_finish_kernel<1>"),
+LAYER_ROLES = [("QKV projection + rotary + KV append", "gemm_ep_kernel<1, 2, 16, 1>"),
                ("attention", "attn_kernel<1, 128, false>"), ("split merge", "attn_combine_kernel<1, 128>"),
-               ("O projection", "gemm_kernel<1, 3"), ("residual + norm (after O)", "resid_kernel<1, 1>"),
-               ("gate/up + SwiGLU", "gemm_swiglu_kernel<1, 2, 16>"), ("down projection", "gemm_kernel<1, 3"),
+               ("O projection + residual + FFN norm sums", "gemm_ep_kernel<1, 2, 16, 2>"),
+               ("gate/up + SwiGLU", "gemm_swiglu_kernel<1, 2, 16, true>"), ("down projection", "gemm_kernel<1, 3"),
                ("residual + norm (after down)", "resid_kernel<1, 1>")]
+NORM_ROLE = len(LAYER_ROLES) - 1   # its grid has one row of workgroups per block row: 33 for T = 33
 
 
 def _short(name: str) -> str:
@@ -364,7 +365,7 @@ def _short(name: str) -> str:
 
 
 def _layer_starts(names):
-    """Indices i where the nine dispatches of a T = 33 layer start."""
+    """Indices i where the dispatches of a T = 33 layer (LAYER_ROLES) start."""
     n = len(LAYER_ROLES)
     return [i for i in range(len(names) - n + 1)
             if all(names[i + j].startswith(p) for j, (_, p) in enumerate(LAYER_ROLES))]
@@ -396,7 +397,7 @@ def rocprof_summary(d: str):
         gy = [int(r["Grid_Size_Y"]) for r in tr]
         t0 = [int(r["Start_Timestamp"]) for r in tr]
         t1 = [int(r["End_Timestamp"]) for r in tr]
-        starts = [i for i in _layer_starts(names) if gy[i + 1] == 33]
+        starts = [i for i in _layer_starts(names) if gy[i + NORM_ROLE] == 33]
         print(f"\nT = 33 layers found: {len(starts)}\n")
         print("| role | kernel | dispatches | median us | mean us |\n|---|---|---|---|---|")
         tot = 0.0
@@ -417,7 +418,7 @@ def rocprof_summary(d: str):
             j = i
             while j < len(names) and names[j] != "result_out_kernel":
                 j += 1
-            if j < len(names) and any(names[x] == "qkv_finish_kernel<1>" and gy[x] == 33 for x in range(i, j)):
+            if j < len(names) and any(names[x] == "resid_kernel<1, 1>" and gy[x] == 33 for x in range(i, j)):
                 b, cur_end = 0, t0[i]
                 for x in range(i, j + 1):
                     s0, s1 = max(t0[x], cur_end), t1[x]

@@ -2452,24 +2452,26 @@ __global__ __launch_bounds__(STREAM_THREADS) void stream_read_kernel(const u32x4
                                                                      unsigned* __restrict__ sink) {
   constexpr int W = STREAM_THREADS / 64;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  // chunk of this workgroup: whole 1 KB segments; the last one also takes
-  // the remainder
+  // chunk of this workgroup: nseg whole 1 KB segments from base (the last
+  // workgroup also reads the segments and 16-byte words left over)
   const size_t seg_all = n16 / 64, per = seg_all / gridDim.x;
-  const size_t s0 = (size_t)blockIdx.x * per, s1 = blockIdx.x + 1 == gridDim.x ? seg_all : s0 + per;
+  const u32x4* base = p + (size_t)blockIdx.x * per * 64;
+  const size_t nseg = blockIdx.x + 1 == gridDim.x ? seg_all - (size_t)blockIdx.x * per : per;
   uint32_t acc = 0;
-  size_t s = s0 + wv;
-  for (; s + (size_t)(STREAM_UNROLL - 1) * W < s1; s += (size_t)STREAM_UNROLL * W) {
+  size_t s = wv;
+  for (; s + (size_t)(STREAM_UNROLL - 1) * W < nseg; s += (size_t)STREAM_UNROLL * W) {
     u32x4 v[STREAM_UNROLL];
 #pragma unroll
-    for (int j = 0; j < STREAM_UNROLL; ++j) v[j] = __builtin_nontemporal_load(p + (s + (size_t)j * W) * 64 + lane);
+    for (int j = 0; j < STREAM_UNROLL; ++j) v[j] = __builtin_nontemporal_load(base + (s + (size_t)j * W) * 64 + lane);
+    __builtin_amdgcn_sched_barrier(0);   // all eight requested before the first is used
 #pragma unroll
     for (int j = 0; j < STREAM_UNROLL; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   }
-  for (; s < s1; s += W) {
-    const u32x4 v = __builtin_nontemporal_load(p + s * 64 + lane);
+  for (; s < nseg; s += W) {
+    const u32x4 v = __builtin_nontemporal_load(base + s * 64 + lane);
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
-  if (blockIdx.x + 1 == gridDim.x)   // the last partial segment
+  if (blockIdx.x + 1 == gridDim.x)   // the words after the last whole segment
     for (size_t i = seg_all * 64 + threadIdx.x; i < n16; i += STREAM_THREADS) {
       const u32x4 v = __builtin_nontemporal_load(p + i);
       acc ^= v.x ^ v.y ^ v.z ^ v.w;
