@@ -120,6 +120,26 @@ def measured_traffic():
     return int(fields["gateup_traffic_bytes_per_launch"])
 
 
+def measured_gap_fraction():
+    """The kernel-gap fraction of the 33-row blocks from the committed
+    rocprofv3 kernel trace, or None if kernels.hip has changed since it was
+    taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "verify_7b_k32_kernel_trace.md")
+    src = os.path.join(ROOT, "paper_2506_02780_amd", "csrc", "kernels.hip")
+    try:
+        text = open(path).read()
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    fields = dict(ln.split(": ", 1) for ln in text.splitlines() if ": " in ln and ln[:1].isalpha())
+    if fields.get("kernels_source_sha256", "").strip() != digest:
+        return None
+    import re
+    m = re.search(r"kernel-gap fraction median ([0-9.]+)", text)
+    return float(m.group(1)) if m else None
+
+
 def cpu_info() -> dict:
     """CPU model and core count of this host."""
     model = "unknown"
@@ -371,6 +391,78 @@ def _layer_starts(names):
             if all(names[i + j].startswith(p) for j, (_, p) in enumerate(LAYER_ROLES))]
 
 
+def _md_rows(text: str) -> dict:
+    """role -> {column: value} from the role tables of a rocprof summary."""
+    rows, hdr = {}, None
+    for ln in text.splitlines():
+        if ln.startswith("| role |"):
+            hdr = [c.strip() for c in ln.strip().strip("|").split("|")][1:]
+        elif ln.startswith("| ") and hdr and not ln.startswith("|---"):
+            cells = [c.strip() for c in ln.strip().strip("|").split("|")]
+            try:
+                rows[cells[0]] = dict(zip(hdr, [float(x) for x in cells[1:1 + len(hdr)]]))
+            except ValueError:
+                pass
+    return rows
+
+
+def counter_table(fetch_dir: str, write_dir: str, mfma_dir: str, trace_dir: str, lm_head_us: float):
+    """The combined per-role table of profiles/verify_7b_k32_counters.md from
+    the four rocprofv3 output directories (FETCH_SIZE, WRITE_SIZE and MFMA
+    counter runs, kernel trace): counters scaled by the 256 MiB calibration
+    copy, algorithmic bytes of the projection model, matrix-core rate at the
+    traced median durations (the LM head's from its ee_time_gemm time) and
+    the MFMA-busy fraction.  Prints to stdout."""
+    import contextlib
+    import io
+    import re
+
+    def summary(d):
+        buf = io.StringIO()
+        with contextlib.redirect_stdout(buf):
+            rocprof_summary(d)
+        return buf.getvalue()
+    ft, wt, mt, tt = (summary(d) for d in (fetch_dir, write_dir, mfma_dir, trace_dir))
+    f, w, m = _md_rows(ft), _md_rows(wt), _md_rows(mt)
+    fcal = float(re.search(r"FETCH_SIZE ([0-9.]+)", ft.split("calibration copy", 1)[1]).group(1))
+    wcal = float(re.search(r"WRITE_SIZE ([0-9.]+)", wt.split("calibration copy", 1)[1]).group(1))
+    fs, ws = 262144 / fcal, 262144 / wcal
+    traced = {}
+    for ln in tt.splitlines():
+        cells = [c.strip() for c in ln.strip().strip("|").split("|")]
+        if len(cells) == 5 and cells[2].isdigit():
+            traced[cells[0]] = float(cells[3])
+    s7 = get_shape_for_table()
+    alg = {LAYER_ROLES[0][0]: projection_model(s7, "qkv", 33)[2],
+           LAYER_ROLES[3][0]: projection_model(s7, "oproj", 33)[2],
+           "gate/up + SwiGLU": projection_model(s7, "gateup", 33)[2],
+           "down projection": projection_model(s7, "down", 33)[2],
+           "LM head (the GEMM before the logits kernel)": projection_model(s7, "lmhead", 33)[2]}
+    print(f"FETCH_SIZE scale {fs:.4f} (copy read 262144 KiB, counter {fcal}); "
+          f"WRITE_SIZE scale {ws:.4f} (counter {wcal})")
+    print("| role | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (scaled) | algorithmic bytes | ratio | "
+          "bf16 MFMA flops | MFMA TFLOP/s at the traced time | MFMA busy |\n|---|---|---|---|---|---|---|---|---|")
+    for role in f:
+        fe, wr = f[role]["FETCH_SIZE"], w[role]["WRITE_SIZE"]
+        hb = (fe * fs + wr * ws) * 1024
+        a = alg.get(role)
+        mm = m[role]
+        fl = mm["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        us = lm_head_us if role.startswith("LM head") else traced.get(role)
+        busy = mm["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / (mm["GRBM_GUI_ACTIVE"] / 8) if mm["GRBM_GUI_ACTIVE"] else 0.0
+        tf = f"{fl / us / 1e6:.1f} ({fl / us / 1e6 / MFMA_BF16_PEAK_TFLOPS:.3f} of peak)" if fl and us else ""
+        name = "LM head" if role.startswith("LM head") else role
+        ab = f"{a / 1e6:.2f} MB | {hb / a:.3f}" if a else " | "
+        print(f"| {name} | {fe:.1f} | {wr:.1f} | {hb / 1e6:.2f} MB | {ab} | "
+              f"{(f'{fl / 1e9:.3f} G' if fl else '0')} | {tf} | {busy:.3f} |")
+
+
+def get_shape_for_table():
+    sys.path.insert(0, ROOT)
+    from workloads import get_shape
+    return get_shape("7b")
+
+
 def rocprof_summary(d: str):
     """Markdown tables from rocprofv3 CSV output under directory d: kernel
     statistics, per-role durations of T = 33 layers, the kernel-gap fraction
@@ -478,6 +570,9 @@ def main():
                     help="only fixed-context verify steps and the projection timing sequences (for rocprofv3)")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--rocprof-summary", metavar="DIR", help="reduce rocprofv3 CSV output in DIR to tables")
+    ap.add_argument("--counter-table", nargs=5, metavar=("FETCH", "WRITE", "MFMA", "TRACE", "LMHEAD_US"),
+                    help="combine the FETCH_SIZE, WRITE_SIZE and MFMA counter runs and the kernel trace into one "
+                         "per-role table (LMHEAD_US: the LM head's ee_time_gemm time)")
     ap.add_argument("--eager", action="store_true", help="launch kernel by kernel (no graph replay)")
     ap.add_argument("--no-33b", action="store_true", help="skip the 33B batch-of-4 measurement")
     ap.add_argument("--no-long", action="store_true", help="skip the long-draft (K = 128..512) measurement")
@@ -485,6 +580,9 @@ def main():
     args = ap.parse_args()
     if args.rocprof_summary:
         rocprof_summary(args.rocprof_summary)
+        return
+    if args.counter_table:
+        counter_table(*args.counter_table[:4], float(args.counter_table[4]))
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -718,7 +816,11 @@ def main():
         "step_hbm": {"algorithmic_bytes": sb["total"], "achieved_GBps": round(sb["total"] / p50 / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / p50 / 1e9 / HBM_PEAK_GBS, 4),
                      "streaming_read_GBps": round(stream_gbps, 1),
-                     "frac_of_streaming_read": round(sb["total"] / p50 / 1e9 / stream_gbps, 4)},
+                     "frac_of_streaming_read": round(sb["total"] / p50 / 1e9 / stream_gbps, 4),
+                     "kernel_gap_fraction": measured_gap_fraction(),
+                     "kernel_gap_note": ("share of a 33-row block's span in which no kernel of it runs, from the "
+                                         "committed rocprofv3 kernel trace of this kernel source (null once "
+                                         "kernels.hip has changed since)")},
         "projections": gemms,
         "roofline": {
             "kernel": f"gemm_swiglu_kernel<{shape.dtype}> (gate/up projection + SwiGLU, T={T})",
