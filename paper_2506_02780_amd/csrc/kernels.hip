@@ -31,6 +31,7 @@ namespace ee {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 
@@ -43,6 +44,34 @@ __device__ __forceinline__ uint32_t f2bf_bits(float f) {
   return u >> 16;
 }
 __device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+// Sum and maximum of x over the lanes l, l ^ 16 (row pairs) or l, l ^ 32
+// (halves) of a wave with v_permlane16_swap / v_permlane32_swap: the swap
+// leaves x[l] and x[l ^ 16] (x[l ^ 32]) in its two results of every lane, in
+// the same order for both lanes of a pair, so the value is that of
+// x + shfl_xor(x, 16) (32) without the LDS round trip.
+__device__ __forceinline__ float xsum16(float x) {
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+__device__ __forceinline__ float xsum32(float x) {
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+__device__ __forceinline__ float xmax16(float x) {
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+__device__ __forceinline__ float xmax32(float x) {
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+// Nearest-even bf16 bits of two finite floats, a in the low half, with one
+// v_cvt_pk_bf16_f32 (equal to f2bf_bits_finite of each, checked for every
+// finite float bit pattern).
+__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
 // Nearest-even bf16 bits of a finite float (no NaN handling, no branch).
 __device__ __forceinline__ uint32_t f2bf_bits_finite(float f) {
   const uint32_t u = __float_as_uint(f);
@@ -1314,6 +1343,16 @@ constexpr int att_qt(bool tree) { return att_threads(tree) / 64 / NSUB; }
 
 // LDS image of one split: K rows [NSUB][64][HD] and V^T [NSUB][HD][64], rows
 // padded by 16 bytes to spread banks.
+// Position, within a bf16 V^T row of the LDS image, of the value of sub-tile
+// key k (0..63).  A PV step's B operand takes keys 32j + 4grp + 0..3 and
+// 32j + 16 + 4grp + 0..3 in MFMA order (the order of the score fragments);
+// storing them side by side lets a lane fetch its value fragment with one
+// 16-byte read, which with the 144-byte row pitch also hits 32 distinct banks
+// per 8 lanes (two 8-byte reads conflicted two-way).  fp32 rows keep key order.
+__host__ __device__ constexpr int vt_pos(int k) {
+  return 32 * (k >> 5) + 8 * ((k >> 2) & 3) + 4 * ((k >> 4) & 1) + (k & 3);
+}
+
 template <int DT, int HD, int THREADS> struct AttnLds {
   static constexpr int ESZ = Geo<DT>::ESZ;
   static constexpr int ROWB = HD * ESZ, KROW = ROWB + 16, VROW = 64 * ESZ + 16;
@@ -1343,17 +1382,31 @@ __device__ __forceinline__ void subtile_scores(const uint4 (&qf)[HD / Geo<DT>::K
     for (int kt = 0; kt < 4; ++kt) sacc[kt] = mma<DT>(kf[kt], qf[s], sacc[kt]);
   }
   m = -INFINITY;
+  // a sub-tile that every column of the wave sees whole (columns past the
+  // block, position -1, hold nothing that is kept) skips the position test:
+  // the same values as with it
+  if (__all(mypos < 0 || base + 63 <= mypos)) {
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kp = base + 16 * kt + 4 * grp + r;
-      const float x = kp <= mypos ? sacc[kt][r] * scale_log2 : -INFINITY;
-      sacc[kt][r] = x;
-      m = fmaxf(m, x);
-    }
-  m = fmaxf(m, __shfl_xor(m, 16));
-  m = fmaxf(m, __shfl_xor(m, 32));
+      for (int r = 0; r < 4; ++r) {
+        const float x = sacc[kt][r] * scale_log2;
+        sacc[kt][r] = x;
+        m = fmaxf(m, x);
+      }
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int kp = base + 16 * kt + 4 * grp + r;
+        const float x = kp <= mypos ? sacc[kt][r] * scale_log2 : -INFINITY;
+        sacc[kt][r] = x;
+        m = fmaxf(m, x);
+      }
+  }
+  m = xmax16(m);
+  m = xmax32(m);
 }
 
 // From the scores and their maximum m: l = sum 2^(s-m) and o += sum 2^(s-m) v
@@ -1369,12 +1422,14 @@ __device__ __forceinline__ void subtile_values(f32x4 (&sacc)[4], float m, VFn vf
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float pv = exp2f(sacc[kt][r] - m_use);   // exp2(-inf) = 0 for hidden keys
+      // v_exp_f32: exp2(-inf) = 0 for hidden keys; a weight below 2^-126
+      // (a score 126 below the maximum) is 0 rather than a denormal
+      const float pv = __builtin_amdgcn_exp2f(sacc[kt][r] - m_use);
       sacc[kt][r] = own ? pv : 0.f;
       l += pv;
     }
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
+  l = xsum16(l);
+  l = xsum32(l);
   // O^T = V^T P^T over the sub-tile's 64 keys
   if (DT == DT_BF16) {
     // P enters the bf16 MFMA as hi + lo bf16 parts (about 16 significant
@@ -1382,17 +1437,15 @@ __device__ __forceinline__ void subtile_values(f32x4 (&sacc)[4], float m, VFn vf
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       vprep(k2);
-      uint32_t ph[8], pl[8];
+      uint32_t ph[4], pl[4];   // packed pairs: elements 2h (low) and 2h + 1
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pv = sacc[2 * k2 + (e >> 2)][e & 3];
-        ph[e] = f2bf_bits_finite(pv);
-        pl[e] = f2bf_bits_finite(pv - bf2f(ph[e]));
+      for (int h = 0; h < 4; ++h) {
+        const float pa = sacc[2 * k2 + (h >> 1)][2 * (h & 1)], pb = sacc[2 * k2 + (h >> 1)][2 * (h & 1) + 1];
+        ph[h] = bf16x2_bits(pa, pb);
+        pl[h] = bf16x2_bits(pa - __uint_as_float(ph[h] << 16), pb - __uint_as_float(ph[h] & 0xffff0000u));
       }
-      const uint4 pfh = make_uint4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
-                                   ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16));
-      const uint4 pfl = make_uint4(pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
-                                   pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16));
+      const uint4 pfh = make_uint4(ph[0], ph[1], ph[2], ph[3]);
+      const uint4 pfl = make_uint4(pl[0], pl[1], pl[2], pl[3]);
       if (STREAMV) {
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
@@ -1515,6 +1568,14 @@ __device__ __forceinline__ void stage_split(const AttnArgs& a, const int* ptable
         }
         v = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
+      if (DT == DT_BF16) {
+        // keys col0 .. col0 + 3 and col0 + 4 .. col0 + 7 to their places
+        const int col0 = (((d - NSUB * LY::KSUB) % LY::VSUB) % VROW) / ESZ;
+        unsigned char* row = lds + d - col0 * ESZ;
+        *reinterpret_cast<uint2*>(row + vt_pos(col0) * ESZ) = make_uint2(v.x, v.y);
+        *reinterpret_cast<uint2*>(row + vt_pos(col0 + 4) * ESZ) = make_uint2(v.z, v.w);
+        continue;
+      }
     }
     *reinterpret_cast<uint4*>(lds + d) = v;
   }
@@ -1624,11 +1685,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   };
   auto vfn = [&](int dt, int j) {
     const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-    if (DT == DT_BF16) {
-      const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
-      const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
-      return make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
+    if (DT == DT_BF16) return *reinterpret_cast<const uint4*>(vr + (32 * j + 8 * grp) * ESZ);   // (vt_pos)
     return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
   };
   subtile_state<DT, HD, false>(qf, kfn, vfn, [](int) {}, base, mypos, a.scale_log2, grp, true, m, l, o);
@@ -1714,7 +1771,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
           const unsigned char* vd = Vall + (16 * dt + c) * VROW;
           auto elt = [&](int i) -> uint32_t {
             const int r = vrow[i];
-            const unsigned char* src = vd + (r >> 6) * LY::VSUB + (r & 63) * ESZ;
+            const unsigned char* src = vd + (r >> 6) * LY::VSUB + (DT == DT_BF16 ? vt_pos(r & 63) : (r & 63)) * ESZ;
             return DT == DT_BF16 ? (uint32_t)*reinterpret_cast<const uint16_t*>(src)
                                  : *reinterpret_cast<const uint32_t*>(src);
           };
@@ -1921,11 +1978,7 @@ __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int
       const unsigned char* Vt = Vall + st * LY::VSUB;
       auto vfn = [&](int dt, int j) {
         const unsigned char* vr = Vt + (size_t)(16 * dt + c) * VROW;
-        if (DT == DT_BF16) {
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr + (32 * j + 4 * grp) * ESZ);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + (32 * j + 16 + 4 * grp) * ESZ);
-          return make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
+        if (DT == DT_BF16) return *reinterpret_cast<const uint4*>(vr + (32 * j + 8 * grp) * ESZ);   // (vt_pos)
         return *reinterpret_cast<const uint4*>(vr + (16 * j + 4 * grp) * ESZ);
       };
       f32x4 oj[ND];
