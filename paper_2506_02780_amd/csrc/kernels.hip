@@ -1501,8 +1501,16 @@ __device__ __forceinline__ void subtile_state(const uint4 (&qf)[HD / Geo<DT>::KS
 // Stage sub-tiles 0 .. nsub-1 of the split starting at position base0 (K rows
 // and V^T, KV head gkv) in LDS with one batch of loads per thread; slots at or
 // past nkeys (not yet written) read as zeros.
+// The NSUB page numbers of the split starting at position base0, with one
+// vector load (scalar loads of the uniform addresses would each wait for the
+// previous one); entries past the table read as 0.
+__device__ __forceinline__ uint4 split_pages(const AttnArgs& a, const int* ptable, int base0) {
+  static_assert(NSUB == 4, "one 16-byte load of page numbers");
+  return bload<0>(make_rsrc(ptable, (unsigned)(a.ptable_len * 4)), (unsigned)((base0 >> 6) * 4));
+}
+
 template <int DT, int HD, int THREADS>
-__device__ __forceinline__ void stage_split(const AttnArgs& a, const int* ptable, int gkv, int base0, int nsub,
+__device__ __forceinline__ void stage_split(const AttnArgs& a, const uint4 p4, int gkv, int base0, int nsub,
                                             int nkeys, unsigned char* lds) {
   using LY = AttnLds<DT, HD, THREADS>;
   constexpr int ESZ = Geo<DT>::ESZ;
@@ -1510,15 +1518,9 @@ __device__ __forceinline__ void stage_split(const AttnArgs& a, const int* ptable
   const size_t layer_bytes = (size_t)a.max_pages * 2 * a.Hkv * 64 * HD * ESZ;
   const auto rs = make_rsrc(a.kv_layer, (unsigned)layer_bytes);
   constexpr int HALF = LY::UNITS / 2;                  // uint4 per K (or V) sub-tile
-  // the split's NSUB page numbers with one vector load (scalar loads of the
-  // uniform addresses would each wait for the previous one)
+  // the split's NSUB page numbers (split_pages)
   int pg[NSUB];
-  {
-    static_assert(NSUB == 4, "one 16-byte load of page numbers");
-    const auto pr = make_rsrc(ptable, (unsigned)(a.ptable_len * 4));
-    const uint4 p4 = bload<0>(pr, (unsigned)((base0 >> 6) * 4));
-    pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
-  }
+  pg[0] = (int)p4.x; pg[1] = (int)p4.y; pg[2] = (int)p4.z; pg[3] = (int)p4.w;
   uint4 tmp[LY::PER];
   unsigned dst[LY::PER];
 #pragma unroll
@@ -1610,10 +1612,15 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   const int* pos = a.pos + rb;
   const unsigned char* path = a.path + (size_t)rb * 64;
   const int* ptable = a.ptable + b * a.ptable_len;
-  // (n, splits in use) with one vector load
+  // (n, splits in use) with one vector load, and the split's page numbers
+  // in the same round trip where the split does not depend on n
   const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
+  uint4 p4 = a.split_mode != 2 ? split_pages(a, ptable, sp * SPLIT) : make_uint4(0u, 0u, 0u, 0u);
   const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
-  if (a.split_mode == 2) sp += (n + 1) / SPLIT;
+  if (a.split_mode == 2) {
+    sp += (n + 1) / SPLIT;
+    p4 = split_pages(a, ptable, sp * SPLIT);
+  }
   if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
   if (a.split_mode == 1 && sp >= (n + 1) / SPLIT) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -1646,7 +1653,7 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   }
 
   // ---- stage every sub-tile of the split with one batch of loads ----
-  stage_split<DT, HD, ATT_THREADS>(a, ptable, gkv, base0, nsub, nkeys, lds);
+  stage_split<DT, HD, ATT_THREADS>(a, p4, gkv, base0, nsub, nkeys, lds);
   __syncthreads();
 
   // A tree row at depth j sits at position n + j and sees, at positions
@@ -1931,6 +1938,7 @@ __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int
   const int* pos = a.pos + rb;
   const int* ptable = a.ptable + b * a.ptable_len;
   const uint2 inf = bload64<0>(make_rsrc(a.info + 4 * b, 8), 0);
+  const uint4 p4 = split_pages(a, ptable, sp * SPLIT);   // (same round trip)
   const int n = __builtin_amdgcn_readfirstlane((int)inf.x);
   if (sp >= __builtin_amdgcn_readfirstlane((int)inf.y)) return;   // the grid covers the longest context
   if (a.split_mode == 1 && sp >= (n + 1) / SPLIT) return;
@@ -1939,7 +1947,7 @@ __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int
   const int nkeys = n + a.T;
   const int base0 = sp * SPLIT;
   const int nsub = min(NSUB, (nkeys - base0 + 63) / 64);
-  stage_split<DT, HD, WIDE_THREADS>(a, ptable, gkv, base0, nsub, nkeys, lds);
+  stage_split<DT, HD, WIDE_THREADS>(a, p4, gkv, base0, nsub, nkeys, lds);
   __syncthreads();
 
   const auto qr = make_rsrc(a.q, (unsigned)((size_t)a.B * a.T * a.H * ROWB));
