@@ -10,15 +10,16 @@
 // on how many other rows share its block; a K = 0 step and a K = 64 step give
 // bitwise-equal rows):
 //   * GEMM: weights are the MFMA A operand (16 output features per tile),
-//     activations the B operand (16 rows per t-tile).  One workgroup owns one
-//     16-feature tile over the whole reduction dimension; its KW waves take
-//     super-steps round-robin and are summed in wave order.
+//     activations the B operand (16 rows per t-tile).  A workgroup's 8 waves
+//     take the super-steps of its part of the reduction round-robin and are
+//     summed in wave order; K slices (down projection, LM head, d > 4096) are
+//     added in slice order by the consuming kernel.
 //   * Attention: keys in splits of 256 absolute positions, each split in
 //     64-position sub-tiles combined by an online softmax in order; splits
 //     merged in order by a second kernel.
 //   * Residual stream, accumulators, softmax and logits are fp32; bf16 models
-//     round the norm outputs, q/k after rotary, v, the attention output and
-//     the SwiGLU product to bf16 (nearest-even).
+//     round the projections' inputs h * gain, q/k after rotary, v, the
+//     attention output and the SwiGLU product to bf16 (nearest-even).
 
 #include "kernels.h"
 
@@ -1064,7 +1065,9 @@ inline bool fused_proj(int d, int qdim, int hd, int dt) {
 // sums of h^2 over the row's 1024-column chunks go to ssq[t][chunk]; the
 // consumer multiplies every output of row t by r = 1 / sqrt(sum h^2 / d + eps)
 // (row_scale), so RMSNorm(h) * gain * W = r * ((h * gain) W).  No workgroup
-// needs a whole row: a row's work spreads over d / 1024 workgroups.
+// needs a whole row: a row's work spreads over d / 1024 workgroups.  (The
+// FFN-side norm of the fused path is instead formed in the O projection's
+// epilogue, with sums of h^2 per 16-column tile: gemm_ep_kernel, ts_rows.)
 
 template <int DT, int MODE>
 __global__ __launch_bounds__(RES_THREADS) void resid_kernel(const void* __restrict__ embed,
