@@ -681,7 +681,10 @@ static hipError_t gemm_swiglu(const uint4* wgu, const uint4* x, int F, int d, in
   int spw = 1;
   while (spw * GEMM_WAVES < a.S) spw *= 2;
   const int ng = fk_groups(R);
-  a.P = ng == 1 ? std::max(1, std::min(256, a.n_pairs)) : std::max(8, 256 / ng / 8 * 8);
+  // one row group: as many workgroups as give each the same count of pairs
+  // (688 pairs: 230 x 3, not 176 x 3 + 80 x 2)
+  const int per_wg = (a.n_pairs + 255) / 256;
+  a.P = ng == 1 ? std::max(1, (a.n_pairs + per_wg - 1) / per_wg) : std::max(8, 256 / ng / 8 * 8);
   const dim3 grid(ng * a.P);
   if (ssqt) {
     if (R <= 16) launch_gemm_swiglu<DT, 1, true>(a, spw, grid, st);
