@@ -56,16 +56,24 @@ def test_long_planted_drafts_accept_exactly(ee):
     eng.close()
 
 
-@pytest.mark.parametrize("width", [512, 4096])
+@pytest.mark.parametrize("width", [512, 4096, 7168])
 def test_long_block_rows_equal_short_block_rows_bitwise(ee, width):
     """Rows of a 401-row block equal the same rows computed one block at a
-    time (K = 0 steps) bit for bit: logits and the committed K/V.  Width 4096
-    (one layer): the projections run two K slices and the gate/up kernel a
-    single pass over d, in 32-row groups at 401 rows and one row alone."""
+    time (K = 0 steps) bit for bit: logits and the committed K/V.  The block's
+    down projection and LM head (and at width 7168 every projection) run in
+    six 80-row groups, the single rows in a launch of one row.  Width 4096
+    (one layer): two K slices in the LM head, and the gate/up kernel a single
+    pass over d, in 32-row groups at 401 rows and one row alone.  Width 7168
+    (one layer): four K slices of 56 super-steps (7 per wave, the eighth slot
+    of each wave zero) in the QKV, O, gate/up projections and the LM head,
+    and a 7-super-step down projection (FFN 224: one wave without
+    super-steps)."""
     if width == 512:
         shape = _bf16_small()
-    else:
+    elif width == 4096:
         shape = _bf16_small(n_layers=1, d_model=4096, n_heads=32, n_kv_heads=8, ffn=2048)
+    else:
+        shape = _bf16_small(n_layers=1, d_model=7168, n_heads=56, n_kv_heads=8, ffn=224)
     w = gen_weights(shape, seed=92, std=0.05 if width == 512 else 0.02)
     prompt = zipf_tokens(shape.vocab, 130, seed=4)
     eng = ee.Engine(shape, w, max_ctx=1024, k_max=512)
