@@ -1597,22 +1597,23 @@ __device__ __forceinline__ void stage_split(const AttnArgs& a, const uint4 p4, i
 // in a fixed order (sub-tile, key tile, key), stored for attn_combine_kernel.
 // A column's arithmetic depends only on the key positions, never on T or on
 // which workgroup ran it; keys it cannot see contribute exact zeros.
+// (the body of one workgroup, block (bx, by, bz) of the grid described
+// above, with its LDS at lds: AttnLds<DT, HD, att_threads(TREE)>::BYTES)
 template <int DT, int HD, bool TREE>
-__global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_block(AttnArgs a, int bx, int by, int bz, unsigned char* lds) {
   constexpr int ATT_THREADS = att_threads(TREE), ATT_QT = att_qt(TREE);
   using LY = AttnLds<DT, HD, ATT_THREADS>;
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
   constexpr int NS = HD / KS;          // fragments along head_dim
   constexpr int ND = HD / 16;          // output dim tiles
   constexpr int ROWB = LY::ROWB, KROW = LY::KROW, VROW = LY::VROW;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[LY::BYTES];
   unsigned char* Kall = lds;
   unsigned char* Vall = lds + NSUB * LY::KSUB;
 
   const int nqt = (a.ncols + 15) / 16;
   const int qgs = (nqt + ATT_QT - 1) / ATT_QT;   // query-tile groups per sequence
-  const int gkv = blockIdx.x, b = blockIdx.z / qgs, qgrp = blockIdx.z % qgs;
-  int sp = blockIdx.y;
+  const int gkv = bx, b = bz / qgs, qgrp = bz % qgs;
+  int sp = by;
   // this sequence's rows, positions, paths, pages and step state
   const int rb = b * a.T;
   const int* pos = a.pos + rb;
@@ -1915,6 +1916,12 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
   }
 }
 
+template <int DT, int HD, bool TREE>
+__global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[AttnLds<DT, HD, att_threads(TREE)>::BYTES];
+  attn_block<DT, HD, TREE>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+}
+
 // Split attention for blocks with many query tiles (long drafts, batches of
 // sequences).  Workgroup (KV head g, split sp, sequence b, group qg of nqg)
 // stages the split once and its 8 waves walk the sequence's query tiles qg*8 +
@@ -1928,18 +1935,19 @@ __global__ __launch_bounds__(att_threads(TREE)) void attn_kernel(AttnArgs a) {
 constexpr int WIDE_THREADS = 512;
 constexpr int WIDE_MIN_QT = 13;   // query tiles per sequence from which the wide kernel is used
 
+// (the body of one workgroup, block (bx, by, bz) of the grid, with its LDS at
+// lds: AttnLds<DT, HD, WIDE_THREADS>::KV_BYTES)
 template <int DT, int HD>
-__global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int nqg) {
+__device__ __forceinline__ void attn_wide_block(AttnArgs a, int nqg, int bx, int by, int bz, unsigned char* lds) {
   using LY = AttnLds<DT, HD, WIDE_THREADS>;
   constexpr int KS = Geo<DT>::KS, EPL = Geo<DT>::EPL, ESZ = Geo<DT>::ESZ;
   constexpr int NS = HD / KS, ND = HD / 16;
   constexpr int ROWB = LY::ROWB, KROW = LY::KROW, VROW = LY::VROW;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[LY::KV_BYTES];
   const unsigned char* Kall = lds;
   const unsigned char* Vall = lds + NSUB * LY::KSUB;
 
   const int nqt = (a.ncols + 15) / 16;
-  const int gkv = blockIdx.x, sp = blockIdx.y, b = blockIdx.z / nqg, qg = blockIdx.z % nqg;
+  const int gkv = bx, sp = by, b = bz / nqg, qg = bz % nqg;
   const int rb = b * a.T;
   const int* pos = a.pos + rb;
   const int* ptable = a.ptable + b * a.ptable_len;
@@ -2019,6 +2027,34 @@ __global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int
         out[HD + 1] = L;
       }
     }
+  }
+}
+
+template <int DT, int HD>
+__global__ __launch_bounds__(WIDE_THREADS) void attn_wide_kernel(AttnArgs a, int nqg) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[AttnLds<DT, HD, WIDE_THREADS>::KV_BYTES];
+  attn_wide_block<DT, HD>(a, nqg, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+}
+
+// A large tree's attention in one launch: first the workgroups of
+// attn_kernel<TREE> over the splits holding the tree's rows (tail: grid
+// Hkv x ty x tz; the longest), then those of attn_wide_kernel over the splits
+// below them (lin: grid Hkv x wy x wz), so the two sets run side by side
+// instead of one after the other.  Every workgroup runs exactly the arithmetic
+// of its own kernel.
+template <int DT, int HD>
+__global__ __launch_bounds__(WIDE_THREADS) void attn_tree_wide_kernel(AttnArgs tail, AttnArgs lin, int nqg,
+                                                                     int ty, int tz, int wy) {
+  static_assert(att_threads(true) == WIDE_THREADS, "one workgroup size for both parts");
+  constexpr int B1 = AttnLds<DT, HD, WIDE_THREADS>::BYTES, B2 = AttnLds<DT, HD, WIDE_THREADS>::KV_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[B1 > B2 ? B1 : B2];
+  const int hk = tail.Hkv, ntree = hk * ty * tz;
+  const int id = blockIdx.x;
+  if (id < ntree) {
+    attn_block<DT, HD, true>(tail, id % hk, id / hk % ty, id / (hk * ty), lds);
+  } else {
+    const int w = id - ntree;
+    attn_wide_block<DT, HD>(lin, nqg, w % hk, w / hk % wy, w / (hk * wy), lds);
   }
 }
 
@@ -2639,20 +2675,24 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
            const bool wide = nqt >= WIDE_MIN_QT;
            if (aa.tree && wide) {
              // a large tree: the splits below its rows hold keys every row sees
-             // unmasked, computed by the wide kernel; the tree kernel takes
-             // only the (at most two) splits holding the tree's rows
+             // unmasked, computed as by the wide kernel; the tree kernel's
+             // workgroups take only the (at most two) splits holding the
+             // tree's rows; both sets in one launch
              static_assert(64 + 1 <= SPLIT, "a tree (at most 64 nodes) spans at most two splits");
              AttnArgs lin = aa;
              lin.tree = 0;
              lin.split_mode = 1;
-             const int per = m.Hkv * nsplit * B;
-             const int nqg = std::max(1, std::min((nqt + 7) / 8, (512 + per - 1) / per));
-             hipLaunchKernelGGL((attn_wide_kernel<DT, HD>), dim3(m.Hkv, nsplit, B * nqg), dim3(WIDE_THREADS), 0, st,
-                                lin, nqg);
              AttnArgs tail = aa;
              tail.split_mode = 2;
-             hipLaunchKernelGGL((attn_kernel<DT, HD, true>), dim3(m.Hkv, std::min(nsplit, 2), B * ((nqt + qt - 1) / qt)),
-                                dim3(att_threads(true)), 0, st, tail);
+             const int ty = std::min(nsplit, 2), tz = B * ((nqt + qt - 1) / qt);
+             // query-tile groups of the wide part: as many as keep the whole
+             // grid within one workgroup per CU (each holds 140 KB of LDS),
+             // counting one split's worth of tree workgroups (the second
+             // exits unless the tree's rows cross a split boundary)
+             const int per = m.Hkv * nsplit * B;
+             const int nqg = std::max(1, std::min((nqt + 7) / 8, (256 - m.Hkv * tz) / per));
+             hipLaunchKernelGGL((attn_tree_wide_kernel<DT, HD>), dim3(m.Hkv * (ty * tz + nsplit * B * nqg)),
+                                dim3(WIDE_THREADS), 0, st, tail, lin, nqg, ty, tz, nsplit);
              return last();
            }
            if (!aa.tree && wide) {
