@@ -109,9 +109,10 @@ def test_tree_verify_matches_oracle(ee, cfg):
 @pytest.mark.parametrize("prompt_len,heads", [(150, 4), (250, 4), (150, 8), (255, 8), (300, 8)])
 def test_tree_rows_equal_chain_rows_bitwise(ee, prompt_len, heads):
     # heads = 8 (4 query heads per KV head): the 64-node tree has 17 query
-    # tiles and runs as a wide launch over the splits below its rows plus the
-    # tree kernel over the splits holding them (from slot n + 1: split 0 at
-    # n = 150, split 1 at n = 255 and 300); the 40-node tree stays in one launch
+    # tiles and runs the wide kernel's work over the splits below its rows and
+    # the tree kernel's over the splits holding them, in one launch (from slot
+    # n + 1: split 0 at n = 150, split 1 at n = 255 and 300); the 40-node tree
+    # runs the tree kernel alone
     shape = _bf16_small() if heads == 4 else _bf16_small(d_model=1024, n_heads=8)
     w = gen_weights(shape, seed=42, std=0.05)
     prompt = zipf_tokens(shape.vocab, prompt_len, seed=13)
