@@ -588,7 +588,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on exactly one GPU: the verification step of one edit session is "
-              "not sharded across GPUs in this build (use --gpus 1)", file=sys.stderr)
+              "not sharded across GPUs (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
