@@ -43,6 +43,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak
 LONG_K = 512                      # longest draft the engine is built for
+CTX_SWEEP = (1024, 2048, 4096, 8000)   # committed lengths of the K = 32 step's context sweep (7B; max_ctx <= 8192)
 # The Reuse driver resumes at a match of at least this many generated tokens;
 # shorter (single-token) matches are frequent by chance and can move the
 # cursor past the true position in the original code.
@@ -603,6 +604,8 @@ def main():
     weights = gen_weights(shape, seed=1234)
     log(f"[bench] weights drawn in {time.perf_counter() - t0:.1f}s")
     max_ctx = max(ctx + args.gen + 66, ctx + LONG_K + 2)
+    if args.config == "7b" and not args.profile_only:
+        max_ctx = max(max_ctx, max(CTX_SWEEP) + K + 2)
     eng = ee.Engine(shape, weights, max_ctx=max_ctx, k_max=LONG_K)
     if args.eager:
         eng.use_graphs(False)
@@ -791,6 +794,27 @@ def main():
 
     edit = None if (args.no_edit or args.config != "7b") else edit_sessions(ee, eng, shape, ctx, first, G, log)
 
+    # the step at several committed lengths (attention's share of the bytes
+    # grows with n): each prompt is prefilled into the sequence afresh, the
+    # draft is K Zipf tokens, the cache is rolled back after every step
+    ctx_sweep = {}
+    for n_ctx in (CTX_SWEEP if args.config == "7b" else ()):
+        eng.rollback(0, 0, -1)
+        f_n = eng.prefill(0, zipf_tokens(shape.vocab, n_ctx, seed=42))
+        d_n = [int(x) for x in zipf_tokens(shape.vocab, K, seed=43)]
+        lat_n = []
+        for i in range(120):
+            eng.rollback(0, n_ctx, f_n)
+            ts = time.perf_counter()
+            eng.verify(0, d_n)
+            if i >= 20:
+                lat_n.append(time.perf_counter() - ts)
+        l50 = float(np.percentile(lat_n, 50))
+        sb_n = step_bytes(shape, K + 1, n_ctx)
+        ctx_sweep[str(n_ctx)] = {"p50_ms": round(l50 * 1e3, 4), "p90_ms": round(float(np.percentile(lat_n, 90)) * 1e3, 4),
+                                 "kv_read_bytes": sb_n["kv_read"], "algorithmic_bytes": sb_n["total"],
+                                 "hbm_frac": round(sb_n["total"] / l50 / 1e9 / HBM_PEAK_GBS, 4)}
+
     result = {
         "metric": METRIC,
         "value": round(emitted / elapsed, 2),
@@ -849,6 +873,8 @@ def main():
         "breakdown_note": ("one K=32 verify at the fixed context, every launch bracketed by HIP events (each figure "
                            "includes ~3-4 us of event overhead per launch; every launch of the block is counted)"),
         "k_sweep_at_ctx": k_sweep,
+        "ctx_sweep_k": ({"k": K, "draft": "K Zipf tokens (the step's cost, not its acceptance)", "by_ctx": ctx_sweep}
+                        if ctx_sweep else None),
         "tree64_at_ctx": tree64,
         "long_drafts_at_ctx": long_drafts or None,
         "entropy_verify_at_ctx": entropy,
