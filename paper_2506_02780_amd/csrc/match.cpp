@@ -20,8 +20,8 @@ extern "C" int32_t ee_match_reuse(const int32_t* generated, int32_t n_gen, const
   for (int32_t len = top; len >= min_ngram; --len) {
     const int32_t* suf = generated + (n_gen - len);
     // window [j, j + len) must end at or after the cursor and leave a draft
-    int32_t j = cursor - len;
-    if (j < 0) j = 0;
+    // (a cursor at or below len puts no bound on j; no overflow for any cursor)
+    int32_t j = cursor <= len ? 0 : cursor - len;
     for (; j + len < n_orig; ++j) {
       int32_t i = 0;
       while (i < len && original[j + i] == suf[i]) ++i;

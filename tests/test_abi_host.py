@@ -82,5 +82,11 @@ def test_matcher_equals_oracle():
         lo = int(g.integers(1, 3))
         hi = int(g.integers(lo, 9))
         assert ee.match_reuse(gen, orig, cur, lo, hi) == match_reuse(gen, orig, cur, lo, hi)
+    # cursors at the ends of the int32 range (no bound / nothing left to draft)
+    for _ in range(200):
+        orig = g.integers(0, 3, int(g.integers(0, 30)))
+        gen = g.integers(0, 3, int(g.integers(1, 8)))
+        for cur in (-2 ** 31, -2 ** 31 + 1, -7, 2 ** 31 - 1):
+            assert ee.match_reuse(gen, orig, cur, 1, 4) == match_reuse(gen, orig, cur, 1, 4)
     a = ctypes.c_int32()
     assert ee.ee_match_reuse_c(None, 0, None, 0, 0, 0, 8, ctypes.byref(a), ctypes.byref(a)) == ee.EE_EINVAL
