@@ -110,7 +110,10 @@ int32_t ee_destroy(ee_ctx* ctx);
  * return the greedy token of the last row in *next_token: the first emitted
  * token of plain greedy decoding (Eq. 1, the argmax of the target's
  * distribution given the prompt), now "pending" (emitted, not yet run through
- * the model).  n >= 1.   */
+ * the model).  n >= 1.  Errors: EE_EINVAL for NULL pointers, n < 1 or a token
+ * outside [0, vocab); EE_ESTATE if the sequence is not empty; EE_ECAPACITY if
+ * n > max_ctx - 1 or the KV pool has too few free pages.  On an error the
+ * sequence stays empty. */
 int32_t ee_prefill(ee_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n,
                    int32_t* next_token);
 
@@ -279,7 +282,8 @@ int32_t ee_match_reuse(const int32_t* generated, int32_t n_gen, const int32_t* o
  * token) are written at out[n_out..n_out+*n_new-1]; out_cap >= n_out +
  * max(k_reuse, gamma) + 1.  With top_k = 0 the output is exactly the target's
  * greedy decoding whatever the draft model proposes.
- * Errors: EE_EINVAL for bad parameters; EE_ESTATE if out does not end with
+ * Errors: EE_EINVAL for bad parameters (a state whose phase is neither
+ * phase or whose cursor is negative among them); EE_ESTATE if out does not end with
  * the target's pending token or the draft sequence does not follow the
  * output; capacity and HIP errors as the calls it makes.  On an error the
  * target sequence is unchanged; the draft sequence is realigned by the next

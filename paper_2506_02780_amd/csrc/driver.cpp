@@ -73,6 +73,7 @@ int32_t ee_edit_step(ee_ctx* target, int32_t seq, ee_ctx* draft, int32_t dseq, c
       p->max_match < p->min_match)
     return EE_EINVAL;
   if (st->phase != EE_PHASE_REUSE && st->phase != EE_PHASE_GENERATE) return EE_EINVAL;
+  if (st->cursor < 0) return EE_EINVAL;   // (the fallback draft starts there: never before original[0])
   if ((int64_t)out_cap < (int64_t)n_out + std::max(p->k_reuse, p->gamma) + 1) return EE_EINVAL;
   int32_t tl, tp, rc;
   if ((rc = state_of(target, seq, &tl, &tp))) return rc;

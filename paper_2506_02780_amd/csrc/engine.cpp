@@ -92,7 +92,7 @@ bool valid_cfg(const ee_model_config* c, std::string* why) {
   if (c->dtype == EE_F32 && c->head_dim != 64) return bad("fp32 models need head_dim 64");
   if (c->n_heads % c->n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
   const int ks = c->dtype == EE_BF16 ? 32 : 16;
-  if (c->d_model > 8192 || c->ffn > 32768 || c->n_heads * c->head_dim > 32768)
+  if (c->d_model > 8192 || c->ffn > 32768 || (int64_t)c->n_heads * c->head_dim > 32768)   // (no int overflow)
     return bad("d_model <= 8192, ffn and n_heads*head_dim <= 32768");
   if (c->d_model % ks || c->ffn % ks || (c->n_heads * c->head_dim) % ks || c->vocab % ks)
     return bad("d_model, ffn, n_heads*head_dim and vocab must be multiples of 32 (bf16) / 16 (f32)");
@@ -808,9 +808,9 @@ int32_t ee_prefill(ee_ctx* c, int32_t seq, const int32_t* tokens, int32_t n, int
   if (n < 1) return fail(c, EE_EINVAL, "prefill needs at least one token");
   Seq& s = c->seqs[seq];
   if (s.live) return fail(c, EE_ESTATE, "sequence already holds tokens (roll it back to 0 first)");
+  if (n > c->cfg.max_ctx - 1) return fail(c, EE_ECAPACITY, "prompt longer than max_ctx - 1");
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, EE_EINVAL, "token outside [0, vocab)");
-  if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "prompt longer than max_ctx - 1");
   int last;
   if ((rc = commit_rows(c, s, tokens, n, &last))) return rc;
   s.live = true;
@@ -1059,7 +1059,7 @@ int32_t ee_load_kv(ee_ctx* c, int32_t seq, int32_t n, int32_t pending, const voi
   if (pending < 0 || pending >= c->cfg.vocab) return fail(c, EE_EINVAL, "pending token outside [0, vocab)");
   Seq& s = c->seqs[seq];
   if (s.live) return fail(c, EE_ESTATE, "sequence already holds tokens (roll it back to 0 first)");
-  if (n + 1 > c->cfg.max_ctx) return fail(c, EE_ECAPACITY, "cache longer than max_ctx - 1");
+  if (n > c->cfg.max_ctx - 1) return fail(c, EE_ECAPACITY, "cache longer than max_ctx - 1");
   if ((rc = order_after_user(c))) return rc;
   int added;
   if (!reserve_pages(c, s, n, &added)) return fail(c, EE_ECAPACITY, "KV pool exhausted");

@@ -54,6 +54,11 @@ def test_config_sizes_and_validation():
     rc = ee.ee_create(ctypes.byref(huge), ctypes.byref(w), 1, 1, 1, None, ctypes.byref(ctx))
     assert rc == ee.EE_EINVAL and b"LM head" in ee.ee_last_error(None)
     assert ee.ee_capture_bytes(ctypes.byref(cfg), 33) > 0 and ee.ee_capture_bytes(ctypes.byref(cfg), 0) == 0
+    # n_heads * head_dim beyond the int range (2^25 x 128 = 2^32) is refused, not wrapped
+    wide = ee.make_config(get_shape("7b", n_heads=2 ** 25, n_kv_heads=2 ** 25), max_ctx=128)
+    assert ee.ee_workspace_bytes(ctypes.byref(wide)) == 0
+    rc = ee.ee_create(ctypes.byref(wide), ctypes.byref(w), 1, 1, 1, None, ctypes.byref(ctx))
+    assert rc == ee.EE_EINVAL and b"n_heads*head_dim" in ee.ee_last_error(None)
 
 
 def test_null_context_calls_fail_cleanly():

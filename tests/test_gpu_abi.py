@@ -52,6 +52,12 @@ def test_capacity_errors_leave_state_unchanged(ee, eng):
     assert eng.seq_state(0) == (196 + a, nxt)
     _expect(ee, ee.EE_ECAPACITY, eng.prefill, 1, zipf_tokens(1024, 250, seed=3))
     assert eng.seq_state(1) == (0, -1)
+    # a length at the top of the int32 range is refused before any token is read
+    import ctypes
+    buf = (ctypes.c_int32 * 4)(1, 2, 3, 4)
+    nx = ctypes.c_int32()
+    assert ee.ee_prefill(eng.ctx, 1, buf, 2 ** 31 - 1, ctypes.byref(nx)) == ee.EE_ECAPACITY
+    assert eng.seq_state(1) == (0, -1)
     eng.rollback(0, 0, -1)
 
 

@@ -126,6 +126,12 @@ def test_edit_session_errors(ee):
     assert e.value.code == ee.EE_EINVAL
     assert tgt.seq_state(0) == before
     s.params.k_reuse = 8
+    s.state.cursor = -1                            # the fallback draft would start before the original
+    with pytest.raises(ee.EEError) as e:
+        s.step()
+    assert e.value.code == ee.EE_EINVAL
+    assert tgt.seq_state(0) == before
+    s.state.cursor = 0
     s.step()
     assert tgt.seq_state(0)[0] > before[0]
     tgt.close()
