@@ -6,7 +6,8 @@ random committed bf16 cache installed with ``ee_load_kv``, and compared with
 the oracle (Eq. 3's forward, Eq. 7's acceptance) on identical inputs:
 
 * 7B (d 4096, 32 / 8 heads, FFN 11008, vocab 32256): layers 0, 15 and 31, a
-  K = 32 block over 2048 committed positions;
+  K = 32 block over 2048 committed positions; layer 15 with a 64-node draft
+  tree (the tree walk and the compacted path checked too);
 * 1B (d 2048, 16 / 4 heads, FFN 5632): layer 7, a K = 16 block over 1024;
 * 33B (d 7168, 56 / 8 heads: 7 query heads per KV head, FFN 19200): layer 30,
   one ``ee_verify_batch`` block of 4 sequences x 65 rows over 4096 committed
@@ -39,9 +40,9 @@ import numpy as np
 import pytest
 
 from helpers import OneLayer, RoundingCheck, deciding_margin, gpu_site_values
-from oracle import OracleSession, greedy_rows
+from oracle import OracleSession, greedy_rows, top2_margin
 from oracle.numerics import to_f64
-from workloads import gen_weights, get_shape, random_kv_context, zipf_tokens
+from workloads import gen_weights, get_shape, random_kv_context, random_tree, zipf_tokens
 
 pytestmark = pytest.mark.gpu
 
@@ -69,18 +70,18 @@ def _install(eng, shape, b, ctx, seed):
     return [(to_f64(k, "bf16"), to_f64(v, "bf16")) for k, v in kv], pending
 
 
-def _compare(shape, w, cache, pending, draft, gpu_logits, gpu_a, gpu_next, sites, gpu_kv, label):
+def _compare(shape, w, cache, pending, draft, gpu_logits, gpu_a, gpu_next, sites, gpu_kv, label, parent=None):
     """Oracle twice: checking and following the GPU's rounding decisions
     (logits within 2e-2 and 1e-4, K/V bitwise), and with its own rounding
-    (the flip cascade: printed, held to 0.1)."""
+    (the flip cascade: printed, held to 0.1).  parent: a draft tree."""
     ref = OracleSession(shape, w)
     ref.set_cache(cache, pending)
-    ra, rn, _ = ref.verify(draft)
+    ra, rn, _ = ref.verify(draft, parent)
     plain = float(np.abs(gpu_logits - ref.last_logits).max())
     chk = RoundingCheck(sites)
     fol = OracleSession(shape, w, rounding=chk)
     fol.set_cache(cache, pending)
-    fa, fn, _ = fol.verify(draft)
+    fa, fn, fpath = fol.verify(draft, parent)
     tight = float(np.abs(gpu_logits - fol.last_logits).max())
     print(f"[fullwidth] {label}: |GPU - oracle| {plain:.4f}, after checked rounding {tight:.2e}; "
           f"{chk.summary()}; accept {gpu_a}/{ra}, next {gpu_next}/{rn}", flush=True)
@@ -89,8 +90,11 @@ def _compare(shape, w, cache, pending, draft, gpu_logits, gpu_a, gpu_next, sites
     assert tight <= TOL and tight <= TIGHT
     assert plain <= LOOSE
     # acceptance, decided on the checked logits: exact wherever the deciding
-    # rows' top-2 margins exceed the remaining difference
-    if deciding_margin(fol.last_logits, fa, len(draft)) > TIGHT:
+    # rows' top-2 margins exceed the remaining difference (a tree walk is
+    # decided by the rows it visits: the pending row and the accepted path)
+    decide = (deciding_margin(fol.last_logits, fa, len(draft)) if parent is None
+              else float(top2_margin(fol.last_logits[[0] + list(fpath)]).min()))
+    if decide > TIGHT:
         assert (gpu_a, gpu_next) == (fa, fn)
     # committed K/V: the pending row and the accepted rows, bit for bit
     n = cache[0][0].shape[0]
@@ -134,6 +138,37 @@ def test_7b_layer_k32_over_2048_positions(ee, layer):
 
 def test_1b_layer_k16_over_1024_positions(ee):
     _single(ee, "1b", 7, 1024, 16, seed=70)
+
+
+def test_7b_layer_tree64_over_2048_positions(ee):
+    """A 64-node draft tree (depth 8, branching 3) at the 7B width over 2048
+    positions: 17 query tiles, so the tree's split and the splits below it run
+    in one launch.  Second block: the root's first child replaced by the
+    greedy token, so the walk accepts at least one node."""
+    shape, w = _case("7b", 15)
+    ctx, k = 2048, 64
+    eng = ee.Engine(shape, w, max_ctx=ctx + k + 8, k_max=k)
+    try:
+        cache, pending = _install(eng, shape, 0, ctx, seed=80)
+        parent = random_tree(k, max_depth=8, max_branch=3, seed=11)
+        draft = zipf_tokens(shape.vocab, k, seed=81)
+        first = int(np.flatnonzero(parent == -1)[0])   # the root's first child
+        for blk in range(2):
+            eng.rollback(0, ctx, pending)
+            eng.capture(k + 1)
+            a, nxt, _ = eng.verify(0, draft, parent)
+            eng.capture(None)
+            lg = eng.logits()
+            sites = gpu_site_values(eng.captured(), shape, slice(0, k + 1))
+            kk, vv = eng.read_kv(0, 0)
+            gkv = (to_f64(kk[ctx:], "bf16"), to_f64(vv[ctx:], "bf16"))
+            fol = _compare(shape, w, cache, pending, draft, lg, a, nxt, sites, gkv,
+                           f"7b layer 15 tree of {k} nodes n={ctx} block {blk}", parent=parent)
+            draft = draft.copy()
+            draft[first] = greedy_rows(fol.last_logits)[0]
+        assert a >= 1
+    finally:
+        eng.close()
 
 
 def test_33b_layer_batch_of_4_k64_over_4096_positions(ee):
