@@ -7,7 +7,8 @@ the oracle (Eq. 3's forward, Eq. 7's acceptance) on identical inputs:
 
 * 7B (d 4096, 32 / 8 heads, FFN 11008, vocab 32256): layers 0, 15 and 31, a
   K = 32 block over 2048 committed positions; layer 15 with a 64-node draft
-  tree (the tree walk and the compacted path checked too);
+  tree (the tree walk and the compacted path checked too); layer 31 with
+  long drafts, K = 128 and 512;
 * 1B (d 2048, 16 / 4 heads, FFN 5632): layer 7, a K = 16 block over 1024;
 * 33B (d 7168, 56 / 8 heads: 7 query heads per KV head, FFN 19200): layer 30,
   one ``ee_verify_batch`` block of 4 sequences x 65 rows over 4096 committed
@@ -138,6 +139,14 @@ def test_7b_layer_k32_over_2048_positions(ee, layer):
 
 def test_1b_layer_k16_over_1024_positions(ee):
     _single(ee, "1b", 7, 1024, 16, seed=70)
+
+
+@pytest.mark.parametrize("k", [128, 512])
+def test_7b_layer_long_draft_over_2048_positions(ee, k):
+    """Long Reuse drafts at the 7B width: the fused projections in 32-row
+    groups (5 and 16 of them), the down projection and LM head in 80-row
+    groups, the wide attention kernel (33 and 129 query tiles)."""
+    _single(ee, "7b", 31, 2048, k, seed=60 + k)
 
 
 def test_7b_layer_tree64_over_2048_positions(ee):
