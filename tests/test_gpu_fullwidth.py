@@ -7,8 +7,9 @@ the oracle (Eq. 3's forward, Eq. 7's acceptance) on identical inputs:
 
 * 7B (d 4096, 32 / 8 heads, FFN 11008, vocab 32256): layers 0, 15 and 31, a
   K = 32 block over 2048 committed positions; layer 15 with a 64-node draft
-  tree (the tree walk and the compacted path checked too); layer 31 with
-  long drafts, K = 128 and 512;
+  tree (the tree walk and the compacted path checked too) and with
+  entropy-aware top-5 verification (every clear threshold compared); layer
+  31 with long drafts, K = 128 and 512;
 * 1B (d 2048, 16 / 4 heads, FFN 5632): layer 7, a K = 16 block over 1024;
 * 33B (d 7168, 56 / 8 heads: 7 query heads per KV head, FFN 19200): layer 30,
   one ``ee_verify_batch`` block of 4 sequences x 65 rows over 4096 committed
@@ -139,6 +140,57 @@ def test_7b_layer_k32_over_2048_positions(ee, layer):
 
 def test_1b_layer_k16_over_1024_positions(ee):
     _single(ee, "1b", 7, 1024, 16, seed=70)
+
+
+def test_7b_layer_entropy_topk_over_2048_positions(ee):
+    """Entropy-aware verification (Eq. 9-10, k = 5) at the 7B width: the
+    block's rounding decisions checked and followed as above, then every
+    threshold tau compared with the oracle's wherever the top-6 logit gaps and
+    k H's distance to an integer exceed the remaining difference, and the
+    outcome where every deciding row is clear.  Second block: the first
+    three draft tokens replaced by their row's second-best token, which
+    Eq. 10 accepts whenever tau >= 2."""
+    from oracle import entropy_threshold
+    shape, w = _case("7b", 15)
+    ctx, k, top = 2048, 32, 5
+    eng = ee.Engine(shape, w, max_ctx=ctx + k + 8, k_max=k)
+    try:
+        cache, pending = _install(eng, shape, 0, ctx, seed=85)
+        draft = zipf_tokens(shape.vocab, k, seed=86)
+        compared = 0
+        for blk in range(2):
+            eng.rollback(0, ctx, pending)
+            eng.capture(k + 1)
+            (a, nxt, thr), = eng.verify_topk([0], [draft], top, True)
+            eng.capture(None)
+            lg = eng.logits()
+            chk = RoundingCheck(gpu_site_values(eng.captured(), shape, slice(0, k + 1)))
+            fol = OracleSession(shape, w, rounding=chk)
+            fol.set_cache(cache, pending)
+            fa, fn, _ = fol.verify_topk(draft, top, True)
+            tight = float(np.abs(lg - fol.last_logits).max())
+            print(f"[fullwidth] 7b layer 15 top-{top} K={k} block {blk}: after checked rounding {tight:.2e}; "
+                  f"{chk.summary()}; accept {a}/{fa}, next {nxt}/{fn}", flush=True)
+            assert chk.mismatches() == 0, chk.summary()
+            assert tight <= TIGHT
+            clear = []
+            for i in range(k + 1):
+                s = np.sort(fol.last_logits[i])[::-1][:top + 1]
+                _, h, tau = entropy_threshold(fol.last_logits[i], top)
+                x = top * h
+                ok = np.min(s[:-1] - s[1:]) > 2 * tight and abs(x - round(x)) > 15 * tight
+                clear.append(ok)
+                if ok and i < k:
+                    assert thr[i] == tau, (blk, i, thr[i], tau)
+                    compared += 1
+            if all(clear[:fa + 1]):
+                assert (a, nxt) == (fa, fn)
+            second = np.argsort(-fol.last_logits, axis=1, kind="stable")[:, 1]
+            draft = draft.copy()
+            draft[:3] = second[:3]
+        assert a >= 1 and compared >= 32
+    finally:
+        eng.close()
 
 
 @pytest.mark.parametrize("k", [128, 512])
