@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import OracleSession, top2_margin
+from oracle.accept import accept_tree
 from oracle.numerics import to_f64
 from workloads import gen_weights, get_shape, random_tree, tree_tokens, zipf_tokens
 
@@ -84,6 +85,10 @@ def test_tree_verify_matches_oracle(ee, cfg):
         lg = eng.logits()
         err = float(np.abs(lg - ref.last_logits).max())
         assert err <= tol, f"step {step}: max |logit difference| {err} > {tol}"
+        # the GPU's walk is exactly the greedy walk over its own logits (lowest
+        # index on ties), at every step
+        ga, gn, gpath = accept_tree(toks, parent, np.argmax(lg, axis=1))
+        assert (a, n, [int(x) + 1 for x in nodes]) == (ga, gn, gpath), f"step {step}: walk"
         same = (a, n) == (ra, rn) and [int(x) + 1 for x in nodes] == list(rpath)
         deciding = float(top2_margin(ref.last_logits)[[0] + list(rpath)].min())
         if not same:
