@@ -711,10 +711,12 @@ inline bool fused_swiglu(int d, int dt) { return d / ks_of(dt) <= FK_MAX_S; }
 //   * EP_RESID (O): a workgroup owns single tiles; the epilogue adds the
 //     projection to the residual stream, stores x = h * gain of the FFN-side
 //     norm (the gate/up projection's packed input) and each row's sum of h^2
-//     over the tile's 16 columns (the row scale's tile sums).
+//     over the tile's 16 columns (the row scale's tile sums);
+//   * EP_STORE (LM head): single tiles, the fp32 products stored as they are
+//     (logits_kernel applies the final norm's row scale).
 // Each output's reduction order depends only on K, never on the block's rows.
 
-enum { EP_ROPE = 1, EP_RESID = 2 };
+enum { EP_ROPE = 1, EP_RESID = 2, EP_STORE = 3 };
 
 struct EpArgs {
   const uint4* w;        // packed weights [n_tiles][S][64]
@@ -738,6 +740,8 @@ struct EpArgs {
   void* xout;            // packed [R][d] output x = h * gain
   int x_S;               // super-steps of d
   float* ssqt;           // [R][n_tiles] per-tile sums of h^2
+  // EP_STORE
+  float* y;              // [R][16 n_tiles] fp32 products
 };
 
 template <int DT, int MTV, int SPW, int EPI>
@@ -805,7 +809,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_ep_kernel(EpArgs a) {
   const int th = a.hd / 16, hp = th / 2;                     // tiles and pairs per head
   auto item_of = [&](int k) { return g + (k / TPI) * a.P; };
   auto tile_of = [&](int k) {
-    if (EPI == EP_RESID) return item_of(k);
+    if (EPI != EP_ROPE) return item_of(k);
     const int p = item_of(k);
     return (p / hp) * th + p % hp + (k & 1) * hp;
   };
@@ -855,7 +859,7 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_ep_kernel(EpArgs a) {
         if (MTV == 2)
           cs1 = bload64<0>(cr, (threadIdx.x < 16 && T > 32) ? (unsigned)(((size_t)spos[32] * (a.hd / 2) + i0 + j) * 8)
                                                             : OOB);
-      } else {
+      } else if (EPI == EP_RESID) {
         const int f = 16 * item_of(k) + f4;
         const auto hr = make_rsrc(a.h, (unsigned)((size_t)a.R * a.d * 4));
         const auto gr = make_rsrc(a.gain, (unsigned)(a.d * 4));
@@ -1018,6 +1022,9 @@ __global__ __launch_bounds__(GEMM_WAVES * 64) void gemm_ep_kernel(EpArgs a) {
           *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.xout) + fi) = make_float4(xo[0], xo[1], xo[2], xo[3]);
         if ((rl >> 4) == 0) a.ssqt[(size_t)row * a.n_tiles + tile] = ss;
       }
+    } else if (EPI == EP_STORE && mine) {
+      const int f = 16 * item_of(k) + 4 * (rl >> 4);
+      *reinterpret_cast<float4*>(a.y + (size_t)row * (16 * a.n_tiles) + f) = make_float4(v[0], v[1], v[2], v[3]);
     }
   }
 }
@@ -1058,6 +1065,10 @@ static hipError_t gemm_ep(EpArgs a, int R, hipStream_t st) {
 inline bool fused_proj(int d, int qdim, int hd, int dt) {
   return d / ks_of(dt) <= FK_MAX_S && qdim / ks_of(dt) <= FK_MAX_S && hd % 32 == 0 && d % 256 == 0 && d <= 4096;
 }
+
+// Whether the LM head runs as gemm_ep_kernel (EP_STORE) rather than with K
+// slices: its reduction over d fits one workgroup.  Depends only on d.
+inline bool lm_head_one_slice(int d, int dt) { return d / ks_of(dt) <= FK_MAX_S; }
 
 // ------------------------------------------------------------ embed / norm --
 
@@ -2776,17 +2787,25 @@ static hipError_t forward_t(const Model& m, const Work& w, const Step& s, Prof* 
     // x_attn of the next layer, or (after the last layer) x_final
     if (s.cap && (e = cap(l + 1, 0, w.xbuf, R16 * d * ESZ)) != hipSuccess) return e;
   }
-  // LM head, logits + chunk maxima, argmax
-  if ((e = timed(prof, PC_LMHEAD, st, [&] { return gemm<DT>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); })) != hipSuccess)
+  // LM head (without K slices when its reduction fits one workgroup), logits
+  // + chunk maxima, argmax
+  const bool lm1 = lm_head_one_slice(d, DT);
+  if ((e = timed(prof, PC_LMHEAD, st, [&] {
+         if (!lm1) return gemm<DT>(m.lm_head, w.xbuf, m.V, d, R, w.part, st);
+         EpArgs la{};
+         la.w = m.lm_head; la.x = w.xbuf; la.S = Sd; la.n_tiles = m.V / 16; la.n_items = m.V / 16; la.y = w.part;
+         return gemm_ep<DT, EP_STORE>(la, R, st);
+       })) != hipSuccess)
     return e;
+  const int sk_lm = lm1 ? 1 : sk_d;
   const int nchunk = (m.V + 2047) / 2048;
   const bool topk = s.mode == 3;
   if ((e = timed(prof, PC_FINISH, st, [&] {
          if (topk)
-           hipLaunchKernelGGL(logits_kernel<true>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
+           hipLaunchKernelGGL(logits_kernel<true>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_lm, R, m.V,
                               w.logits, w.amax, nchunk, w.ssq, d, m.eps);
          else
-           hipLaunchKernelGGL(logits_kernel<false>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_d, R, m.V,
+           hipLaunchKernelGGL(logits_kernel<false>, dim3(nchunk, R), dim3(256), 0, st, w.part, sk_lm, R, m.V,
                               w.logits, w.amax, nchunk, w.ssq, d, m.eps);
          return last();
        })) != hipSuccess)
@@ -2898,8 +2917,17 @@ hipError_t run_gemm_sequence(const Model& m, const Work& w, int which, int R, hi
         break;
       case PC_DOWN: e = bf ? gemm<DT_BF16>(lp.wd, w.zbuf, d, m.F, R, w.part, st)
                            : gemm<DT_F32>(lp.wd, w.zbuf, d, m.F, R, w.part, st); break;
-      case PC_LMHEAD: e = bf ? gemm<DT_BF16>(m.lm_head, w.xbuf, m.V, d, R, w.part, st)
-                             : gemm<DT_F32>(m.lm_head, w.xbuf, m.V, d, R, w.part, st); break;
+      case PC_LMHEAD:
+        if (lm_head_one_slice(d, m.dt)) {
+          EpArgs la{};
+          la.w = m.lm_head; la.x = w.xbuf; la.S = d / ks; la.n_tiles = m.V / 16; la.n_items = m.V / 16;
+          la.y = w.part;
+          e = bf ? gemm_ep<DT_BF16, EP_STORE>(la, R, st) : gemm_ep<DT_F32, EP_STORE>(la, R, st);
+        } else {
+          e = bf ? gemm<DT_BF16>(m.lm_head, w.xbuf, m.V, d, R, w.part, st)
+                 : gemm<DT_F32>(m.lm_head, w.xbuf, m.V, d, R, w.part, st);
+        }
+        break;
       default: break;
     }
     if (e != hipSuccess) return e;
