@@ -549,8 +549,10 @@ def rocprof_summary(d: str):
             if starts:
                 print(f"| {role} | " + " | ".join(f"{st.mean(val(ids[k + j], c) for k in starts):.1f}"
                                                   for c in counters) + " |")
-        lm = [k for k in range(len(names) - 1)
-              if names[k].startswith("gemm_kernel<1, 3") and names[k + 1].startswith("logits_kernel")]
+        # the LM head: the dispatch after a block's last T = 33 layer, when the
+        # logits kernel follows it
+        nl = len(LAYER_ROLES)
+        lm = [s + nl for s in starts if s + nl + 1 < len(names) and names[s + nl + 1].startswith("logits_kernel")]
         if lm:
             print("| LM head (the GEMM before the logits kernel) | " + " | ".join(
                 f"{st.mean(val(ids[k], c) for k in lm):.1f}" for c in counters) + " |")
